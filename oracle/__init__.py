@@ -1,0 +1,140 @@
+"""DO-loss reference oracle -- TEST INFRASTRUCTURE ONLY.
+
+Plain CPU implementation (``doloss_oracle.c``) of what the DO-loss hot path
+computes, written from the paper's definitions (arXiv 2609.32398):
+
+* ``topk_signature``  -- Sec. 3.1.1, Eq. (1): the dense bool matrix F[E][N] of
+  Top-K token assignments (ties to the lower expert index, -0 == +0, NaN
+  ranks below -inf and NaNs tie).
+* ``pack``            -- the binary load signature of each expert as 64-bit
+  words, token t -> word t//64, bit t%64, tail bits zero.
+* ``hamming``         -- Eq. (6) G_ij = ||F_i - F_j||_1 from its definition.
+* ``loss``            -- Eq. (3) sum_{i!=j} G_ij^2 (fp64 and exact integer),
+  with mean and population variance of the off-diagonal distances
+  (App. C.1).
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may use this package.  It shares no code with the HIP library.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "doloss_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+F32, BF16 = 0, 1
+
+
+class _LossResult(ctypes.Structure):
+    _fields_ = [("sum", ctypes.c_uint64), ("sumsq", ctypes.c_uint64), ("loss", ctypes.c_double),
+                ("mean", ctypes.c_double), ("var", ctypes.c_double)]
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (-O2, OpenMP; portable x86-64 code)."""
+    global _lib
+    if not force and os.path.exists(_LIB_PATH):
+        return _LIB_PATH
+    tmp = _LIB_PATH + ".tmp"
+    subprocess.run(["gcc", "-O2", "-fPIC", "-shared", "-fopenmp", "-std=c11", _SRC, "-o", tmp, "-lm"], check=True)
+    os.replace(tmp, _LIB_PATH)
+    _lib = None
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            build()
+        lib = ctypes.CDLL(_LIB_PATH)
+        i64, i32, vp = ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p
+        lib.oracle_topk_signature.argtypes = [vp, ctypes.c_int, i64, i32, i32, vp, ctypes.c_int]
+        lib.oracle_pack.argtypes = [vp, i64, i32, vp]
+        lib.oracle_hamming.argtypes = [vp, i64, i32, vp, ctypes.c_int]
+        lib.oracle_loss.argtypes = [vp, i32, ctypes.POINTER(_LossResult)]
+        for f in ("oracle_topk_signature", "oracle_pack", "oracle_hamming", "oracle_loss"):
+            getattr(lib, f).restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def threads() -> int:
+    """Host threads the oracle uses (all available cores, capped at 16)."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def _dtype_of(scores: np.ndarray) -> int:
+    if scores.dtype == np.float32:
+        return F32
+    if scores.dtype == np.uint16:
+        return BF16
+    raise TypeError("scores must be float32 values or uint16 bf16 bit patterns")
+
+
+def topk_signature(scores: np.ndarray, k: int, nthreads: int | None = None) -> np.ndarray:
+    """Eq. (1): dense F[E][N] (uint8 0/1) for scores of shape (N, E)."""
+    scores = np.ascontiguousarray(scores)
+    N, E = scores.shape
+    F = np.empty((E, N), dtype=np.uint8)
+    rc = _load().oracle_topk_signature(scores.ctypes.data, _dtype_of(scores), N, E, k, F.ctypes.data,
+                                       nthreads or threads())
+    if rc:
+        raise ValueError(f"oracle_topk_signature: bad arguments N={N} E={E} k={k}")
+    return F
+
+
+def pack(F: np.ndarray) -> np.ndarray:
+    """Signature words[E][ceil(N/64)] (uint64) of a dense F[E][N]."""
+    F = np.ascontiguousarray(F, dtype=np.uint8)
+    E, N = F.shape
+    W = (N + 63) // 64
+    words = np.empty((E, W), dtype=np.uint64)
+    _load().oracle_pack(F.ctypes.data, N, E, words.ctypes.data)
+    return words
+
+
+def hamming(F: np.ndarray, nthreads: int | None = None) -> np.ndarray:
+    """Eq. (6) G_ij = ||F_i - F_j||_1 as uint32 D[E][E]."""
+    F = np.ascontiguousarray(F, dtype=np.uint8)
+    E, N = F.shape
+    D = np.empty((E, E), dtype=np.uint32)
+    rc = _load().oracle_hamming(F.ctypes.data, N, E, D.ctypes.data, nthreads or threads())
+    if rc:
+        raise ValueError("oracle_hamming: bad arguments")
+    return D
+
+
+def loss(D: np.ndarray) -> dict:
+    """Eq. (3) and statistics of the off-diagonal distances."""
+    D = np.ascontiguousarray(D, dtype=np.uint32)
+    E = D.shape[0]
+    r = _LossResult()
+    _load().oracle_loss(D.ctypes.data, E, ctypes.byref(r))
+    return dict(sum=int(r.sum), sumsq=int(r.sumsq), loss=float(r.loss), mean=float(r.mean), var=float(r.var))
+
+
+def run(scores: np.ndarray, k: int, nthreads: int | None = None):
+    """Whole path for one layer: (F, words, D, loss dict)."""
+    F = topk_signature(scores, k, nthreads)
+    D = hamming(F, nthreads)
+    return F, pack(F), D, loss(D)
+
+
+def run_stream(micro_batches, k: int, nthreads: int | None = None):
+    """Streaming history: the micro-batches' tokens concatenated in order, then the whole path."""
+    Fs = [topk_signature(s, k, nthreads) for s in micro_batches]
+    F = np.concatenate(Fs, axis=1)
+    D = hamming(F, nthreads)
+    return F, pack(F), D, loss(D)

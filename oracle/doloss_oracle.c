@@ -1,0 +1,161 @@
+/*
+ * DO-loss reference oracle -- TEST INFRASTRUCTURE ONLY.
+ *
+ * A plain, slow, obviously correct CPU implementation of what the DO-loss hot
+ * path computes.  Only the test suite, the smoke check and the CPU-baseline
+ * leg of the benchmark may load it; the product library never does.  It
+ * shares no code, header, table or helper with the HIP implementation.
+ *
+ * Paper: "Function Over Form: Distributional Orthogonalization in
+ * Mixture-of-Experts with Replica Expert Mechanism" (arXiv 2609.32398).
+ * Notation: the paper's m tokens / n experts / K selections are N / E / k here.
+ *
+ *   oracle_topk_signature  Sec. 3.1.1, Eq. (1): f_it = 1 iff expert i is among
+ *                          the Top-K of token t.  Dense bool matrix F[E][N].
+ *   oracle_pack            the binary load signature F_i as 64-bit words
+ *                          (token t -> word t/64, bit t%64, tail bits 0).
+ *   oracle_hamming         Eq. (6) magnitude term G_ij = ||F_i - F_j||_1,
+ *                          computed from the definition as a count of
+ *                          differing positions (not via the Gram identity).
+ *   oracle_loss            Eq. (3): L_origin_DO = sum_{i != j} G_ij^2, with the
+ *                          mean and population variance of the off-diagonal
+ *                          distances (Sec. 3.1.1 / App. C.1: minimising the sum
+ *                          of squares under the fixed total is minimising the
+ *                          variance).  fp64 accumulation, plus exact u64 sums.
+ *
+ * Readings where the paper is silent (each listed in the design notes):
+ *   - ties in Top-K go to the lower expert index;
+ *   - -0.0 equals +0.0 (IEEE comparison);
+ *   - NaN ranks below every number including -inf, and all NaNs tie;
+ *   - scores are ranked as given (no gating function is applied);
+ *   - bf16 scores are widened exactly to fp32 (bits << 16) before comparing.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORACLE_F32 0
+#define ORACLE_BF16 1
+
+typedef struct {
+  uint64_t sum;   /* exact sum over i != j of D_ij */
+  uint64_t sumsq; /* exact sum over i != j of D_ij^2 (Eq. 3) */
+  double loss;    /* Eq. (3) accumulated in fp64 */
+  double mean;    /* sum / (E(E-1)) */
+  double var;     /* population variance of the off-diagonal D_ij, two-pass fp64 */
+} oracle_loss_result;
+
+static double score_at(const void* scores, int dtype, int64_t idx) {
+  if (dtype == ORACLE_F32) return (double)((const float*)scores)[idx];
+  uint32_t bits = (uint32_t)((const uint16_t*)scores)[idx] << 16;
+  float f;
+  memcpy(&f, &bits, 4);
+  return (double)f;
+}
+
+/* Does expert a (value va) outrank expert b (value vb) for the same token? */
+static int outranks(double va, int a, double vb, int b) {
+  int na = isnan(va), nb = isnan(vb);
+  if (na && nb) return a < b;
+  if (na) return 0;
+  if (nb) return 1;
+  if (va > vb) return 1;
+  if (va < vb) return 0;
+  return a < b; /* equal values (this includes -0.0 == +0.0) */
+}
+
+/*
+ * Eq. (1): for every token, pick k experts one at a time, each time the best
+ * not yet chosen under `outranks`.  F must hold E*N bytes; F[e*N + t] is 0/1.
+ */
+int oracle_topk_signature(const void* scores, int dtype, int64_t N, int32_t E, int32_t k, uint8_t* F,
+                          int nthreads) {
+  if (N < 0 || E < 1 || k < 1 || k > E) return -1;
+  memset(F, 0, (size_t)E * (size_t)N);
+#pragma omp parallel num_threads(nthreads > 0 ? nthreads : 1)
+  {
+    double* v = (double*)malloc(sizeof(double) * (size_t)E);
+    uint8_t* chosen = (uint8_t*)malloc((size_t)E);
+#pragma omp for schedule(static)
+    for (int64_t t = 0; t < N; ++t) {
+      for (int32_t e = 0; e < E; ++e) {
+        v[e] = score_at(scores, dtype, t * E + e);
+        chosen[e] = 0;
+      }
+      for (int32_t r = 0; r < k; ++r) {
+        int32_t best = -1;
+        for (int32_t e = 0; e < E; ++e) {
+          if (chosen[e]) continue;
+          if (best < 0 || outranks(v[e], e, v[best], best)) best = e;
+        }
+        chosen[best] = 1;
+        F[(int64_t)best * N + t] = 1;
+      }
+    }
+    free(v);
+    free(chosen);
+  }
+  return 0;
+}
+
+/* Pack F[E][N] into words[E][ceil(N/64)]. */
+int oracle_pack(const uint8_t* F, int64_t N, int32_t E, uint64_t* words) {
+  int64_t W = (N + 63) / 64;
+  memset(words, 0, sizeof(uint64_t) * (size_t)E * (size_t)W);
+  for (int32_t e = 0; e < E; ++e)
+    for (int64_t t = 0; t < N; ++t)
+      if (F[(int64_t)e * N + t]) words[(int64_t)e * W + t / 64] |= (uint64_t)1 << (t % 64);
+  return 0;
+}
+
+/* Eq. (6): D_ij = sum_t |f_it - f_jt| = number of tokens where exactly one of i, j is selected. */
+int oracle_hamming(const uint8_t* F, int64_t N, int32_t E, uint32_t* D, int nthreads) {
+  if (N < 0 || E < 1) return -1;
+  int64_t npairs = (int64_t)E * E;
+#pragma omp parallel for schedule(dynamic, 1) num_threads(nthreads > 0 ? nthreads : 1)
+  for (int64_t p = 0; p < npairs; ++p) {
+    int32_t i = (int32_t)(p / E), j = (int32_t)(p % E);
+    if (j < i) continue;
+    const uint8_t* fi = F + (int64_t)i * N;
+    const uint8_t* fj = F + (int64_t)j * N;
+    uint64_t d = 0;
+    for (int64_t t = 0; t < N; ++t) d += (uint64_t)(fi[t] != fj[t]);
+    D[(int64_t)i * E + j] = (uint32_t)d;
+    D[(int64_t)j * E + i] = (uint32_t)d;
+  }
+  return 0;
+}
+
+/* Eq. (3) and the statistics of the off-diagonal distances. */
+int oracle_loss(const uint32_t* D, int32_t E, oracle_loss_result* out) {
+  if (E < 1) return -1;
+  memset(out, 0, sizeof(*out));
+  if (E == 1) return 0;
+  uint64_t s1 = 0, s2 = 0;
+  double f2 = 0.0, f1 = 0.0;
+  for (int32_t i = 0; i < E; ++i)
+    for (int32_t j = 0; j < E; ++j) {
+      if (i == j) continue;
+      uint64_t d = D[(int64_t)i * E + j];
+      s1 += d;
+      s2 += d * d;
+      f1 += (double)d;
+      f2 += (double)d * (double)d;
+    }
+  double P = (double)E * (double)(E - 1);
+  double mean = f1 / P;
+  double acc = 0.0;
+  for (int32_t i = 0; i < E; ++i)
+    for (int32_t j = 0; j < E; ++j) {
+      if (i == j) continue;
+      double dev = (double)D[(int64_t)i * E + j] - mean;
+      acc += dev * dev;
+    }
+  out->sum = s1;
+  out->sumsq = s2;
+  out->loss = f2;
+  out->mean = mean;
+  out->var = acc / P;
+  return 0;
+}
