@@ -1,0 +1,264 @@
+#!/usr/bin/env python3
+"""Benchmark of the DO-loss hot path on one MI355X.
+
+One step = one do_fused call over the whole workload already resident in HBM:
+router Top-K -> signatures (written out) -> E x E Hamming -> loss, for every
+layer.  Prints ONE JSON line (rank 0, one GPU).
+
+Default workload: 8 layers x 4,194,304 tokens, 256 experts, top-8, fp32
+scores drawn as a per-token softmax with clustered expert preferences.
+``--workload 3`` times the streaming history instead (16 micro-batches of
+65,536 tokens appended into one 1,048,576-token history, then finalised).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
+
+
+def log(msg: str):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", type=int, default=4, choices=[1, 2, 3, 4])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-tokens", type=int, default=1 << 20)
+    ap.add_argument("--layers", type=int, default=None, help="override the layer count (testing only)")
+    return ap.parse_args()
+
+
+def ensure_built():
+    import paper_2609_32398_amd.hipbuild as hb
+
+    if not os.path.exists(hb.LIB_PATH):
+        import __graft_entry__
+
+        __graft_entry__.build()
+
+
+def pinned_host(n, E, dtype_code):
+    import torch
+
+    tdt = torch.float32 if dtype_code == 0 else torch.int16
+    return torch.empty((n, E), dtype=tdt, pin_memory=True)
+
+
+def upload_workload(cfg: int, layers: int):
+    """Generate the workload layer by layer on the host and copy it into one device buffer."""
+    import numpy as np
+    import torch
+
+    import synth
+
+    w = synth.WORKLOADS[cfg]
+    N, E = w["n"], w["E"]
+    tdt = torch.float32 if w["dtype"] == 0 else torch.bfloat16
+    dev = torch.empty((layers, N, E), dtype=tdt, device="cuda")
+    host = pinned_host(N, E, w["dtype"])
+    hview = host.numpy() if w["dtype"] == 0 else host.numpy().view(np.uint16)
+    t0 = time.time()
+    for l in range(layers):
+        synth.workload_fill(cfg, l, out=hview)
+        dev[l].copy_(host.view(tdt) if w["dtype"] == 1 else host)
+        log(f"generated layer {l + 1}/{layers} ({time.time() - t0:.1f} s)")
+    torch.cuda.synchronize()
+    return dev
+
+
+def cpu_baseline(cfg: int, n_tokens: int):
+    """The oracle as it stands on a bounded sample of the same workload (rank 0 only)."""
+    import oracle
+    import synth
+
+    w = synth.WORKLOADS[cfg]
+    n = min(n_tokens, w["n"])
+    x = synth.workload_fill(cfg, 0, 0, n)
+    th = oracle.threads()
+    t0 = time.perf_counter()
+    F = oracle.topk_signature(x, w["k"], th)
+    D = oracle.hamming(F, th)
+    oracle.loss(D)
+    dt = time.perf_counter() - t0
+    return dict(value=n / dt, unit="tokens/s", cores=th, kind="oracle",
+                sample=f"layer 0, first {n} tokens of the workload (top-k, Hamming, loss; {dt:.2f} s)")
+
+
+def bench_layers(args, cfg):
+    import torch
+
+    import paper_2609_32398_amd as dl
+    import synth
+
+    w = synth.WORKLOADS[cfg]
+    L = args.layers or w["layers"]
+    N, E, k = w["n"], w["E"], w["k"]
+    scores = upload_workload(cfg, L)
+    bits = dl.alloc_bits(L, N, E, scores.device)
+    D = dl.alloc_D(L, E, scores.device)
+    out = dl.alloc_out(L, scores.device)
+
+    def step():
+        dl.do_fused(scores, k, bits=bits, D=D, out=out)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ks = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    for a, b in ks:  # materialise the events so their handles exist
+        a.record()
+        b.record()
+    torch.cuda.synchronize()
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_stop = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t_start.record()
+    for a, b in ks:
+        dl.do_profile_next(a, b)
+        step()
+    t_stop.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = t_start.elapsed_time(t_stop)
+    kern_ms = sum(a.elapsed_time(b) for a, b in ks) / len(ks)
+    ms_per_step = total_ms / args.steps
+    tokens = L * N
+    elem = 4 if w["dtype"] == 0 else 2
+    bytes_per_token = E * elem + E // 8
+    alg_bytes = tokens * bytes_per_token
+    rec = dl.loss_records(out)
+    res = dict(
+        metric="DO-loss tokens/s per layer (top-k→signature→E×E Hamming→loss); % of HBM peak",
+        value=tokens / (ms_per_step / 1e3),
+        unit="tokens/s",
+        n_gpus=1,
+        steps=args.steps,
+        warmup=args.warmup,
+        ms_per_step=ms_per_step,
+        higher_is_better=True,
+        scaling="weak",
+        vs_baseline=None,
+        dtype="i32",
+        data="synthetic",
+        config=dict(workload=w["name"], layers=L, tokens_per_layer=N, experts=E, k=k,
+                    score_dtype="f32" if w["dtype"] == 0 else "bf16", signatures_written=True),
+        roofline=dict(bound="hbm", achieved=alg_bytes / (kern_ms / 1e3) / 1e9, peak=HBM_PEAK_GBS, unit="GB/s",
+                      frac=alg_bytes / (kern_ms / 1e3) / 1e9 / HBM_PEAK_GBS, traffic=None,
+                      kernel="k_topk (fused top-k + signature + popcount Gram)", kernel_ms=kern_ms,
+                      algorithmic_bytes=alg_bytes, bytes_per_token=bytes_per_token),
+        step_gbs=alg_bytes / (ms_per_step / 1e3) / 1e9,
+        wall_s_timed=wall,
+        check=dict(layer0_sum=rec[0]["sum"], expected_sum=2 * N * k * (E - k)),
+    )
+    assert rec[0]["sum"] == 2 * N * k * (E - k), "zero-sum identity (Eq. 2) violated"
+    return res
+
+
+def bench_stream(args):
+    import numpy as np
+    import torch
+
+    import paper_2609_32398_amd as dl
+    import synth
+
+    cfg = 3
+    w = synth.WORKLOADS[cfg]
+    nmb, N, E, k = w["layers"], w["n"], w["E"], w["k"]
+    copies = 2  # two distinct sets of 16 buffers defeat the 256 MB last-level cache
+    host = pinned_host(N, E, 1)
+    hview = host.numpy().view(np.uint16)
+    bufs = []
+    for c in range(copies):
+        row = []
+        for b in range(nmb):
+            synth.workload_fill(cfg, b, out=hview)
+            t = torch.empty((N, E), dtype=torch.bfloat16, device="cuda")
+            t.copy_(host.view(torch.bfloat16))
+            row.append(t)
+        bufs.append(row)
+    log("streaming micro-batches uploaded")
+    s = dl.DoStream(E, k, nmb * N)
+    D = torch.empty((E, E), dtype=torch.int32, device="cuda")
+    out = dl.alloc_out(1, "cuda")
+
+    def step(i):
+        s.reset()
+        s.append_many(bufs[i % copies])
+        s.finalize(D, out)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    ks = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    for a, b in ks:
+        a.record()
+        b.record()
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_stop = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record()
+    for i, (a, b) in enumerate(ks):
+        s.reset()
+        dl.do_profile_next(a, b)
+        s.append_many(bufs[i % copies])
+        s.finalize(D, out)
+    t_stop.record()
+    torch.cuda.synchronize()
+    ms_per_step = t_start.elapsed_time(t_stop) / args.steps
+    kern_ms = sum(a.elapsed_time(b) for a, b in ks) / len(ks)
+    tokens = nmb * N
+    bytes_per_token = E * 2 + E // 8
+    alg = tokens * bytes_per_token
+    rec = dl.loss_records(out)[0]
+    assert rec["sum"] == 2 * tokens * k * (E - k)
+    s.close()
+    return dict(
+        metric="DO-loss tokens/s per layer (top-k→signature→E×E Hamming→loss); % of HBM peak",
+        value=tokens / (ms_per_step / 1e3), unit="tokens/s", n_gpus=1, steps=args.steps, warmup=args.warmup,
+        ms_per_step=ms_per_step, higher_is_better=True, scaling="weak", vs_baseline=None, dtype="i32",
+        data="synthetic",
+        config=dict(workload=w["name"], micro_batches=nmb, tokens_per_micro_batch=N, experts=E, k=k,
+                    score_dtype="bf16", buffer_sets=copies),
+        roofline=dict(bound="hbm", achieved=alg / (kern_ms / 1e3) / 1e9, peak=HBM_PEAK_GBS, unit="GB/s",
+                      frac=alg / (kern_ms / 1e3) / 1e9 / HBM_PEAK_GBS, traffic=None,
+                      kernel="k_topk (stream append, 16 micro-batches per launch)", kernel_ms=kern_ms,
+                      algorithmic_bytes=alg, bytes_per_token=bytes_per_token),
+    )
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
+              "(the distances are additive over token shards; see the design notes).", file=sys.stderr)
+        sys.exit(2)
+    ensure_built()
+    import torch
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    import paper_2609_32398_amd as dl
+
+    dl.lib()
+    cfg = args.workload
+    res = bench_stream(args) if cfg == 3 else bench_layers(args, cfg)
+    if not args.no_cpu_baseline:
+        log("timing the oracle on the host")
+        res["cpu_baseline"] = cpu_baseline(cfg, args.cpu_sample_tokens)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,178 @@
+/*
+ * doloss.h -- C ABI of the DO-loss hot path on MI355X (gfx950).
+ *
+ * DO-loss ("Function Over Form: Distributional Orthogonalization in
+ * Mixture-of-Experts with Replica Expert Mechanism", arXiv 2609.32398)
+ * records, for every expert, which tokens of a batch routed to it (its binary
+ * load signature) and penalises overlap between experts through the pairwise
+ * Hamming distances of those signatures.  This library computes, on one GPU:
+ *
+ *   1. router Top-K over a token x expert score matrix          (Sec. 3.1.1, Eq. 1)
+ *   2. the per-expert N-bit load signatures F_i                  (Sec. 3.1.1)
+ *   3. the E x E matrix G_ij = ||F_i - F_j||_1                    (Sec. 3.1.3, Eq. 6)
+ *   4. the loss sum_{i != j} G_ij^2 with mean / variance of the
+ *      off-diagonal distances                                   (Sec. 3.1.1, Eq. 3; App. C.1)
+ *
+ * Notation: the paper's m tokens / n experts / K choices are N / E / k here.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Every pointer argument is DEVICE memory of the current HIP device unless
+ *   stated otherwise; the caller owns it.  Only do_stream_create allocates.
+ * - Calls are asynchronous on `stream` (0 = the null stream).  Results are
+ *   valid once the caller synchronises that stream.
+ * - Every argument is validated on the host before anything is launched; on
+ *   error nothing is enqueued and a do_status other than DO_OK is returned.
+ *   do_last_error() gives a message for the calling thread's last error.
+ * - Layouts (all row-major, little-endian):
+ *     scores  [L][N][E]  fp32 or bf16 (raw bf16 bit patterns)
+ *     bits    [L][E][W]  uint64, W = ceil(N / 64); token t of expert e is bit
+ *                        (t % 64) of word t / 64 (least significant bit first);
+ *                        bits past N are zero
+ *     D       [L][E][E]  uint32, symmetric, zero diagonal
+ *     out     [L]        do_loss_result
+ * - Ranking rule for Top-K (the paper gives none; see the design notes):
+ *   larger score first; equal scores go to the lower expert index; -0.0 and
+ *   +0.0 are equal; NaN ranks below every number (including -inf) and all NaNs
+ *   are equal.  Scores are ranked exactly as given: no gating is applied.
+ * - Limits: 1 <= E <= 1024, 1 <= k <= E, 1 <= N < 2^32, 1 <= L <= 65535 and
+ *   E*(E-1)*N^2 < 2^64 (so the sum of squares is exact in 64 bits).
+ *   The fast path needs 16-byte aligned scores with E*sizeof(score) a multiple
+ *   of 16, E <= 256 and k <= 8; other valid shapes take a slower exact path.
+ */
+#ifndef DOLOSS_H
+#define DOLOSS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  DO_OK = 0,
+  DO_ERR_INVALID_ARG = 1,       /* null/misaligned pointer, size or range out of limits */
+  DO_ERR_UNSUPPORTED_DTYPE = 2, /* dtype is not DO_F32 or DO_BF16 */
+  DO_ERR_CAPACITY = 3,          /* a stream append would exceed the history capacity */
+  DO_ERR_OVERFLOW = 4,          /* E*(E-1)*N^2 >= 2^64 or N >= 2^32 */
+  DO_ERR_HIP = 5                /* the HIP runtime reported an error */
+} do_status;
+
+typedef enum { DO_F32 = 0, DO_BF16 = 1 } do_dtype;
+
+/* Per-layer result of the loss (device memory, 40 bytes). */
+typedef struct {
+  uint64_t sum;   /* exact sum over i != j of D_ij (Eq. 2: equals 2*N*k*(E-k)) */
+  uint64_t sumsq; /* exact sum over i != j of D_ij^2 (Eq. 3) */
+  double loss;    /* Eq. 3 as fp64: L_origin_DO = sum_{i != j} ||F_i - F_j||_1^2 */
+  double mean;    /* sum / (E*(E-1)) */
+  double var;     /* population variance of the E*(E-1) off-diagonal D_ij (App. C.1) */
+} do_loss_result;
+
+/*
+ * Steps 1-2 (Sec. 3.1.1, Eq. 1): Top-k of every token's scores and the packed
+ * load signatures.
+ *   scores  [L][N][E] device, dtype `dtype`
+ *   bits    [L][E][ceil(N/64)] device, fully overwritten
+ */
+do_status do_topk_signature(const void* scores, do_dtype dtype, int64_t N, int32_t E, int32_t k, int32_t L,
+                            uint64_t* bits, hipStream_t stream);
+
+/*
+ * Step 3 (Sec. 3.1.3, Eq. 6 magnitude term; App. C.3 identity): the Hamming
+ * distance matrix of existing signatures, computed as
+ * D_ij = c_ii + c_jj - 2 c_ij with c_ij = popcount(F_i AND F_j).
+ *   bits  [L][E][ceil(N/64)] device; bits past N must be zero (else the
+ *         result is undefined)
+ *   D     [L][E][E] device, fully overwritten
+ */
+do_status do_pairwise_hamming(const uint64_t* bits, int64_t N, int32_t E, int32_t L, uint32_t* D,
+                              hipStream_t stream);
+
+/*
+ * Step 4 (Sec. 3.1.1, Eq. 3; App. C.1): loss and off-diagonal statistics of
+ * any E x E distance matrices (the diagonal is ignored; symmetry is not
+ * assumed).  For E = 1 every field is zero.
+ *   D    [L][E][E] device
+ *   out  [L] device
+ */
+do_status do_loss(const uint32_t* D, int32_t E, int32_t L, do_loss_result* out, hipStream_t stream);
+
+/*
+ * Steps 1-4 in a single pass over the scores: signatures stay on chip and are
+ * written out only if `bits` is not NULL; the co-occurrence counts are
+ * accumulated in `D` itself, which is then turned into distances and reduced
+ * to the loss.  Results are identical to do_topk_signature +
+ * do_pairwise_hamming + do_loss.
+ *   bits  nullable, [L][E][ceil(N/64)] device
+ *   D     [L][E][E] device, fully overwritten
+ *   out   [L] device
+ */
+do_status do_fused(const void* scores, do_dtype dtype, int64_t N, int32_t E, int32_t k, int32_t L, uint64_t* bits,
+                   uint32_t* D, do_loss_result* out, hipStream_t stream);
+
+/*
+ * Streaming global-batch history (Sec. 3.1.4: distances over a batch wider
+ * than one micro-batch; App. F.2, Table 4: G over gradient-accumulated
+ * micro-batches).  A handle owns a
+ * signature history of `capacity_tokens` bits per expert and the running
+ * co-occurrence counts.  Each append ranks one micro-batch and appends its
+ * signatures after the tokens already held (concatenation), so that after any
+ * sequence of appends the distances equal those of one batch made of all
+ * appended tokens in order.
+ */
+typedef struct do_stream_s do_stream;
+
+/* Allocates the history (E x ceil(capacity/64) words) and the counters on the
+ * current device and zeroes them (synchronously).  *out receives the handle. */
+do_status do_stream_create(int32_t E, int32_t k, int64_t capacity_tokens, do_stream** out);
+
+/* Appends n_tokens >= 0 tokens of scores [n_tokens][E] (device).  Fails with
+ * DO_ERR_CAPACITY, leaving the handle unchanged, if the history would overflow. */
+do_status do_stream_append(do_stream* h, const void* scores, do_dtype dtype, int64_t n_tokens, hipStream_t stream);
+
+/* Appends `count` (1..64) micro-batches of n_tokens_each tokens in one launch.
+ * `scores` is a HOST array of `count` device pointers, read during the call. */
+do_status do_stream_append_many(do_stream* h, const void* const* scores, do_dtype dtype, int64_t n_tokens_each,
+                                int32_t count, hipStream_t stream);
+
+/* Writes the distances D [E][E] and the loss `out` [1] (both device) of all
+ * tokens appended so far.  The handle is not modified. */
+do_status do_stream_finalize(do_stream* h, uint32_t* D, do_loss_result* out, hipStream_t stream);
+
+/* Clears the history and the counters (enqueued on `stream`). */
+do_status do_stream_reset(do_stream* h, hipStream_t stream);
+
+/* Frees the handle (synchronises the device first).  NULL is accepted. */
+do_status do_stream_destroy(do_stream* h);
+
+/* Device pointer to the history [E][do_stream_words_per_expert(h)]; bits past
+ * do_stream_tokens(h) are zero. */
+const uint64_t* do_stream_bits(const do_stream* h);
+int64_t do_stream_tokens(const do_stream* h);
+int64_t do_stream_words_per_expert(const do_stream* h);
+
+/*
+ * Benchmark hook: the next do_fused / do_topk_signature / do_stream_append*
+ * call made by this thread records `start` on its stream right before its
+ * main score-streaming kernel and `stop` right after it (one-shot; both are
+ * events of the current device created by the caller).  Pass NULLs to
+ * cancel.  Lets a caller time that kernel alone with hipEventElapsedTime.
+ */
+do_status do_profile_next(hipEvent_t start, hipEvent_t stop);
+
+/* Text of a status code, and the message of the calling thread's last error. */
+const char* do_status_string(do_status s);
+const char* do_last_error(void);
+
+/* Library version as major*10000 + minor*100 + patch. */
+int32_t do_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DOLOSS_H */

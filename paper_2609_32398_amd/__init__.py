@@ -1,0 +1,255 @@
+"""DO-loss hot path on MI355X: Python binding of the C ABI in include/doloss.h.
+
+Argument marshalling only: every step of the path runs in the HIP kernels of
+``libdoloss.so``.  torch is used for device memory and the current stream.
+There is no CPU fallback; if the library is missing the import of the
+binding's functions raises.
+
+Functions keep the C names:
+
+* ``do_topk_signature(scores, k)``  -> bits  [L][E][ceil(N/64)] int64 (uint64 bit patterns)
+* ``do_pairwise_hamming(bits, N)``   -> D     [L][E][E] int32 (uint32 values)
+* ``do_loss(D)``                     -> out   [L][5] (sum, sumsq, loss, mean, var) as a dict list
+* ``do_fused(scores, k, want_bits)`` -> (bits or None, D, out)
+* ``DoStream``                       -> streaming history (do_stream_*)
+
+``scores`` is a CUDA tensor of shape [N, E] or [L, N, E], float32 or bfloat16.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+from .hipbuild import LIB_PATH, build  # noqa: F401
+
+DO_OK, DO_ERR_INVALID_ARG, DO_ERR_UNSUPPORTED_DTYPE, DO_ERR_CAPACITY, DO_ERR_OVERFLOW, DO_ERR_HIP = range(6)
+DO_F32, DO_BF16 = 0, 1
+
+LOSS_RESULT_BYTES = 40
+LOSS_FIELDS = ("sum", "sumsq", "loss", "mean", "var")
+
+
+class DoLossError(RuntimeError):
+    def __init__(self, status: int, where: str, msg: str):
+        super().__init__(f"{where}: status {status} ({msg})")
+        self.status = status
+
+
+_lib = None
+
+
+def lib():
+    """The loaded libdoloss.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
+        st = ctypes.c_int
+        sigs = {
+            "do_topk_signature": ([vp, st, i64, i32, i32, i32, vp, vp], st),
+            "do_pairwise_hamming": ([vp, i64, i32, i32, vp, vp], st),
+            "do_loss": ([vp, i32, i32, vp, vp], st),
+            "do_fused": ([vp, st, i64, i32, i32, i32, vp, vp, vp, vp], st),
+            "do_stream_create": ([i32, i32, i64, ctypes.POINTER(vp)], st),
+            "do_stream_append": ([vp, vp, st, i64, vp], st),
+            "do_stream_append_many": ([vp, ctypes.POINTER(vp), st, i64, i32, vp], st),
+            "do_stream_finalize": ([vp, vp, vp, vp], st),
+            "do_stream_reset": ([vp, vp], st),
+            "do_stream_destroy": ([vp], st),
+            "do_stream_bits": ([vp], vp),
+            "do_stream_tokens": ([vp], i64),
+            "do_stream_words_per_expert": ([vp], i64),
+            "do_status_string": ([st], ctypes.c_char_p),
+            "do_last_error": ([], ctypes.c_char_p),
+            "do_version": ([], i32),
+            "do_profile_next": ([vp, vp], st),
+        }
+        for name, (args, res) in sigs.items():
+            f = getattr(L, name)
+            f.argtypes = args
+            f.restype = res
+        _lib = L
+    return _lib
+
+
+_hip = None
+
+
+def _hip_copy_d2d(dst: int, src: int, nbytes: int) -> int:
+    """Device-to-device copy on the current stream through the HIP runtime torch loaded."""
+    global _hip
+    if _hip is None:
+        _hip = ctypes.CDLL("libamdhip64.so.7")
+        _hip.hipMemcpyAsync.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int,
+                                        ctypes.c_void_p]
+        _hip.hipMemcpyAsync.restype = ctypes.c_int
+    rc = _hip.hipMemcpyAsync(dst, src, nbytes, 3, _stream())  # 3 = hipMemcpyDeviceToDevice
+    return DO_OK if rc == 0 else DO_ERR_HIP
+
+
+def _check(status: int, where: str):
+    if status != DO_OK:
+        raise DoLossError(status, where, lib().do_last_error().decode())
+
+
+def _stream() -> ctypes.c_void_p:
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return DO_F32
+    if t.dtype == torch.bfloat16:
+        return DO_BF16
+    raise TypeError(f"unsupported score dtype {t.dtype}")
+
+
+def _scores_3d(scores: torch.Tensor):
+    if not scores.is_cuda:
+        raise ValueError("scores must be a device tensor")
+    if not scores.is_contiguous():
+        raise ValueError("scores must be contiguous")
+    if scores.dim() == 2:
+        return 1, scores.shape[0], scores.shape[1]
+    if scores.dim() == 3:
+        return scores.shape[0], scores.shape[1], scores.shape[2]
+    raise ValueError("scores must be [N, E] or [L, N, E]")
+
+
+def loss_records(out: torch.Tensor) -> list[dict]:
+    """Decode a [L, 40] uint8 tensor of do_loss_result records."""
+    raw = out.detach().cpu().contiguous().view(torch.uint8).numpy().reshape(-1, LOSS_RESULT_BYTES)
+    recs = []
+    for r in raw:
+        u = r[:16].view("<u8")
+        d = r[16:].view("<f8")
+        recs.append(dict(sum=int(u[0]), sumsq=int(u[1]), loss=float(d[0]), mean=float(d[1]), var=float(d[2])))
+    return recs
+
+
+def alloc_bits(L: int, N: int, E: int, device) -> torch.Tensor:
+    return torch.empty((L, E, (N + 63) // 64), dtype=torch.int64, device=device)
+
+
+def alloc_D(L: int, E: int, device) -> torch.Tensor:
+    return torch.empty((L, E, E), dtype=torch.int32, device=device)
+
+
+def alloc_out(L: int, device) -> torch.Tensor:
+    return torch.empty((L, LOSS_RESULT_BYTES), dtype=torch.uint8, device=device)
+
+
+def do_topk_signature(scores: torch.Tensor, k: int, bits: torch.Tensor | None = None) -> torch.Tensor:
+    L, N, E = _scores_3d(scores)
+    if bits is None:
+        bits = alloc_bits(L, N, E, scores.device)
+    _check(lib().do_topk_signature(scores.data_ptr(), _dtype_code(scores), N, E, k, L, bits.data_ptr(), _stream()),
+           "do_topk_signature")
+    return bits
+
+
+def do_pairwise_hamming(bits: torch.Tensor, N: int, D: torch.Tensor | None = None) -> torch.Tensor:
+    if bits.dim() == 2:
+        bits = bits.unsqueeze(0)
+    L, E, _ = bits.shape
+    if D is None:
+        D = alloc_D(L, E, bits.device)
+    _check(lib().do_pairwise_hamming(bits.data_ptr(), N, E, L, D.data_ptr(), _stream()), "do_pairwise_hamming")
+    return D
+
+
+def do_loss(D: torch.Tensor, out: torch.Tensor | None = None) -> torch.Tensor:
+    if D.dim() == 2:
+        D = D.unsqueeze(0)
+    L, E, _ = D.shape
+    if out is None:
+        out = alloc_out(L, D.device)
+    _check(lib().do_loss(D.data_ptr(), E, L, out.data_ptr(), _stream()), "do_loss")
+    return out
+
+
+def do_fused(scores: torch.Tensor, k: int, want_bits: bool = False, bits: torch.Tensor | None = None,
+             D: torch.Tensor | None = None, out: torch.Tensor | None = None):
+    L, N, E = _scores_3d(scores)
+    if want_bits and bits is None:
+        bits = alloc_bits(L, N, E, scores.device)
+    if D is None:
+        D = alloc_D(L, E, scores.device)
+    if out is None:
+        out = alloc_out(L, scores.device)
+    _check(lib().do_fused(scores.data_ptr(), _dtype_code(scores), N, E, k, L,
+                          bits.data_ptr() if bits is not None else None, D.data_ptr(), out.data_ptr(), _stream()),
+           "do_fused")
+    return bits, D, out
+
+
+def do_profile_next(start: "torch.cuda.Event | None", stop: "torch.cuda.Event | None"):
+    """Bracket the main kernel of this thread's next call with two (recorded-once) torch events."""
+    a = ctypes.c_void_p(start.cuda_event) if start is not None else None
+    b = ctypes.c_void_p(stop.cuda_event) if stop is not None else None
+    _check(lib().do_profile_next(a, b), "do_profile_next")
+
+
+class DoStream:
+    """Streaming global-batch signature history (do_stream_*)."""
+
+    def __init__(self, E: int, k: int, capacity_tokens: int):
+        h = ctypes.c_void_p()
+        _check(lib().do_stream_create(E, k, capacity_tokens, ctypes.byref(h)), "do_stream_create")
+        self.h, self.E, self.k, self.capacity = h, E, k, capacity_tokens
+
+    def append(self, scores: torch.Tensor):
+        _, N, E = _scores_3d(scores)
+        _check(lib().do_stream_append(self.h, scores.data_ptr(), _dtype_code(scores), N, _stream()),
+               "do_stream_append")
+
+    def append_many(self, score_list):
+        ptrs = (ctypes.c_void_p * len(score_list))(*[s.data_ptr() for s in score_list])
+        _, N, _ = _scores_3d(score_list[0])
+        _check(lib().do_stream_append_many(self.h, ptrs, _dtype_code(score_list[0]), N, len(score_list), _stream()),
+               "do_stream_append_many")
+
+    def finalize(self, D: torch.Tensor | None = None, out: torch.Tensor | None = None):
+        dev = torch.device("cuda", torch.cuda.current_device())
+        if D is None:
+            D = torch.empty((self.E, self.E), dtype=torch.int32, device=dev)
+        if out is None:
+            out = alloc_out(1, dev)
+        _check(lib().do_stream_finalize(self.h, D.data_ptr(), out.data_ptr(), _stream()), "do_stream_finalize")
+        return D, out
+
+    def reset(self):
+        _check(lib().do_stream_reset(self.h, _stream()), "do_stream_reset")
+
+    @property
+    def tokens(self) -> int:
+        return int(lib().do_stream_tokens(self.h))
+
+    @property
+    def words_per_expert(self) -> int:
+        return int(lib().do_stream_words_per_expert(self.h))
+
+    def bits_ptr(self) -> int:
+        return int(lib().do_stream_bits(self.h) or 0)
+
+    def history(self) -> torch.Tensor:
+        """Copy of the signature history [E][words_per_expert] (int64 words)."""
+        W = self.words_per_expert
+        out = torch.empty((self.E, W), dtype=torch.int64, device=torch.device("cuda", torch.cuda.current_device()))
+        _check(_hip_copy_d2d(out.data_ptr(), self.bits_ptr(), self.E * W * 8), "history copy")
+        return out
+
+    def close(self):
+        if self.h is not None and self.h.value:
+            _check(lib().do_stream_destroy(self.h), "do_stream_destroy")
+        self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,322 @@
+// Host side of the C ABI declared in include/doloss.h: argument validation,
+// dispatch to the kernels, and the streaming-history handles.
+#include <cstring>
+#include <string>
+
+#include "common.h"
+
+#define DOLOSS_API extern "C" __attribute__((visibility("default")))
+
+using dol::u64;
+
+namespace {
+
+thread_local std::string g_last_error;
+thread_local hipEvent_t g_prof_start = nullptr;
+thread_local hipEvent_t g_prof_stop = nullptr;
+
+// Records the one-shot profiling events around the main kernel launch `f`.
+template <typename F>
+hipError_t profiled(hipStream_t s, F&& f) {
+  hipEvent_t a = g_prof_start, b = g_prof_stop;
+  g_prof_start = g_prof_stop = nullptr;
+  if (a) {
+    const hipError_t e = hipEventRecord(a, s);
+    if (e != hipSuccess) return e;
+  }
+  const hipError_t e = f();
+  if (e != hipSuccess) return e;
+  if (b) return hipEventRecord(b, s);
+  return hipSuccess;
+}
+
+do_status fail(do_status st, const std::string& msg) {
+  g_last_error = msg;
+  return st;
+}
+
+do_status hip_status(hipError_t e, const char* where) {
+  if (e == hipSuccess) return DO_OK;
+  g_last_error = std::string(where) + ": " + hipGetErrorString(e);
+  return DO_ERR_HIP;
+}
+
+size_t dtype_size(do_dtype dt) { return dt == DO_F32 ? 4 : 2; }
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+do_status check_dtype(int dt) {
+  if (dt != DO_F32 && dt != DO_BF16) return fail(DO_ERR_UNSUPPORTED_DTYPE, "dtype must be DO_F32 or DO_BF16");
+  return DO_OK;
+}
+
+// Shape checks shared by every entry point.
+do_status check_shape(int64_t N, int32_t E, int32_t L) {
+  if (E < 1 || E > dol::kMaxE) return fail(DO_ERR_INVALID_ARG, "E must be in [1, 1024]");
+  if (L < 1 || L > 65535) return fail(DO_ERR_INVALID_ARG, "L must be in [1, 65535]");
+  if (N < 1) return fail(DO_ERR_INVALID_ARG, "N must be >= 1");
+  if (N >= (int64_t(1) << 32)) return fail(DO_ERR_OVERFLOW, "N must be < 2^32 (distances are uint32)");
+  const unsigned __int128 s2max = (unsigned __int128)(uint64_t)E * (uint64_t)(E - 1) * (uint64_t)N * (uint64_t)N;
+  if (s2max >> 64) return fail(DO_ERR_OVERFLOW, "E*(E-1)*N^2 must be < 2^64 (exact sum of squares)");
+  return DO_OK;
+}
+
+do_status check_k(int32_t k, int32_t E) {
+  if (k < 1 || k > E) return fail(DO_ERR_INVALID_ARG, "k must be in [1, E]");
+  return DO_OK;
+}
+
+do_status check_scores(const void* scores, do_dtype dt) {
+  if (scores == nullptr) return fail(DO_ERR_INVALID_ARG, "scores is NULL");
+  if (!aligned(scores, dtype_size(dt))) return fail(DO_ERR_INVALID_ARG, "scores is not aligned to its element size");
+  return DO_OK;
+}
+
+bool fast_layout(const void* scores, do_dtype dt, int32_t E) {
+  return aligned(scores, 16) && ((int64_t)E * (int64_t)dtype_size(dt)) % 16 == 0;
+}
+
+#define DO_TRY(expr)                 \
+  do {                               \
+    const do_status st_ = (expr);    \
+    if (st_ != DO_OK) return st_;    \
+  } while (0)
+
+// Top-K over L layers of [N][E] scores, batched up to kMaxSeg layers per launch.
+do_status run_layers(const void* scores, do_dtype dt, int64_t N, int32_t E, int32_t k, int32_t L, u64* bits,
+                     uint32_t* cacc, hipStream_t s) {
+  const int64_t W = (N + 63) / 64;
+  const bool fast = fast_layout(scores, dt, E);
+  dol::PathArgs a{};
+  a.E = E;
+  a.k = k;
+  a.bits = bits;
+  a.bits_layer_words = (int64_t)E * W;
+  a.W = W;
+  a.or_partial = 0;
+  a.cacc = cacc;
+  a.cacc_layer_elems = (int64_t)E * E;
+  const size_t layer_bytes = (size_t)N * (size_t)E * dtype_size(dt);
+  for (int32_t l0 = 0; l0 < L; l0 += dol::kMaxSeg) {
+    const int nseg = (L - l0) < dol::kMaxSeg ? (L - l0) : dol::kMaxSeg;
+    dol::SegTable tab{};
+    for (int i = 0; i < nseg; ++i) {
+      tab.s[i].scores = static_cast<const unsigned char*>(scores) + (size_t)(l0 + i) * layer_bytes;
+      tab.s[i].n = N;
+      tab.s[i].tok_off = 0;
+      tab.s[i].layer = l0 + i;
+    }
+    DO_TRY(hip_status(profiled(s, [&] { return dol::launch_topk(dt, tab, nseg, N, a, fast, s); }), "top-k launch"));
+  }
+  return DO_OK;
+}
+
+}  // namespace
+
+struct do_stream_s {
+  int32_t E;
+  int32_t k;
+  int64_t capacity;
+  int64_t W;
+  int64_t tokens;
+  u64* hist;
+  uint32_t* cacc;
+  int device;
+};
+
+DOLOSS_API const char* do_status_string(do_status s) {
+  switch (s) {
+    case DO_OK: return "DO_OK";
+    case DO_ERR_INVALID_ARG: return "DO_ERR_INVALID_ARG";
+    case DO_ERR_UNSUPPORTED_DTYPE: return "DO_ERR_UNSUPPORTED_DTYPE";
+    case DO_ERR_CAPACITY: return "DO_ERR_CAPACITY";
+    case DO_ERR_OVERFLOW: return "DO_ERR_OVERFLOW";
+    case DO_ERR_HIP: return "DO_ERR_HIP";
+  }
+  return "DO_ERR_UNKNOWN";
+}
+
+DOLOSS_API const char* do_last_error(void) { return g_last_error.c_str(); }
+
+DOLOSS_API int32_t do_version(void) { return 100; }
+
+DOLOSS_API do_status do_profile_next(hipEvent_t start, hipEvent_t stop) {
+  g_prof_start = start;
+  g_prof_stop = stop;
+  return DO_OK;
+}
+
+DOLOSS_API do_status do_topk_signature(const void* scores, do_dtype dtype, int64_t N, int32_t E, int32_t k,
+                                       int32_t L, uint64_t* bits, hipStream_t stream) {
+  DO_TRY(check_dtype(dtype));
+  DO_TRY(check_shape(N, E, L));
+  DO_TRY(check_k(k, E));
+  DO_TRY(check_scores(scores, dtype));
+  if (bits == nullptr || !aligned(bits, 8)) return fail(DO_ERR_INVALID_ARG, "bits is NULL or not 8-byte aligned");
+  return run_layers(scores, dtype, N, E, k, L, reinterpret_cast<u64*>(bits), nullptr, stream);
+}
+
+DOLOSS_API do_status do_pairwise_hamming(const uint64_t* bits, int64_t N, int32_t E, int32_t L, uint32_t* D,
+                                         hipStream_t stream) {
+  DO_TRY(check_shape(N, E, L));
+  if (bits == nullptr || !aligned(bits, 8)) return fail(DO_ERR_INVALID_ARG, "bits is NULL or not 8-byte aligned");
+  if (D == nullptr || !aligned(D, 4)) return fail(DO_ERR_INVALID_ARG, "D is NULL or not 4-byte aligned");
+  const int64_t W = (N + 63) / 64;
+  DO_TRY(hip_status(dol::launch_fill_u32(D, (int64_t)L * E * E, 0u, stream), "fill"));
+  DO_TRY(hip_status(dol::launch_gram_bits(reinterpret_cast<const u64*>(bits), W, E, L, D, stream), "gram"));
+  return hip_status(dol::launch_finalize(D, D, nullptr, E, L, stream), "finalize");
+}
+
+DOLOSS_API do_status do_loss(const uint32_t* D, int32_t E, int32_t L, do_loss_result* out, hipStream_t stream) {
+  DO_TRY(check_shape(1, E, L));
+  if (D == nullptr || !aligned(D, 4)) return fail(DO_ERR_INVALID_ARG, "D is NULL or not 4-byte aligned");
+  if (out == nullptr || !aligned(out, 8)) return fail(DO_ERR_INVALID_ARG, "out is NULL or not 8-byte aligned");
+  return hip_status(dol::launch_loss(D, E, L, out, stream), "loss");
+}
+
+DOLOSS_API do_status do_fused(const void* scores, do_dtype dtype, int64_t N, int32_t E, int32_t k, int32_t L,
+                              uint64_t* bits, uint32_t* D, do_loss_result* out, hipStream_t stream) {
+  DO_TRY(check_dtype(dtype));
+  DO_TRY(check_shape(N, E, L));
+  DO_TRY(check_k(k, E));
+  DO_TRY(check_scores(scores, dtype));
+  if (bits != nullptr && !aligned(bits, 8)) return fail(DO_ERR_INVALID_ARG, "bits is not 8-byte aligned");
+  if (D == nullptr || !aligned(D, 4)) return fail(DO_ERR_INVALID_ARG, "D is NULL or not 4-byte aligned");
+  if (out == nullptr || !aligned(out, 8)) return fail(DO_ERR_INVALID_ARG, "out is NULL or not 8-byte aligned");
+  if (E > dol::kFastMaxE && bits == nullptr)
+    return fail(DO_ERR_INVALID_ARG, "do_fused needs a bits buffer when E > 256");
+  DO_TRY(hip_status(dol::launch_fill_u32(D, (int64_t)L * E * E, 0u, stream), "fill"));
+  if (E <= dol::kFastMaxE) {
+    DO_TRY(run_layers(scores, dtype, N, E, k, L, reinterpret_cast<u64*>(bits), D, stream));
+  } else {
+    DO_TRY(run_layers(scores, dtype, N, E, k, L, reinterpret_cast<u64*>(bits), nullptr, stream));
+    DO_TRY(hip_status(dol::launch_gram_bits(reinterpret_cast<const u64*>(bits), (N + 63) / 64, E, L, D, stream),
+                      "gram"));
+  }
+  return hip_status(dol::launch_finalize(D, D, out, E, L, stream), "finalize");
+}
+
+DOLOSS_API do_status do_stream_create(int32_t E, int32_t k, int64_t capacity_tokens, do_stream** out) {
+  if (out == nullptr) return fail(DO_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  DO_TRY(check_shape(capacity_tokens, E, 1));
+  DO_TRY(check_k(k, E));
+  do_stream* h = new do_stream_s{};
+  h->E = E;
+  h->k = k;
+  h->capacity = capacity_tokens;
+  h->W = (capacity_tokens + 63) / 64;
+  h->tokens = 0;
+  hipError_t e = hipGetDevice(&h->device);
+  if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&h->hist), (size_t)E * h->W * sizeof(u64));
+  if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&h->cacc), (size_t)E * E * sizeof(uint32_t));
+  if (e == hipSuccess) e = hipMemset(h->hist, 0, (size_t)E * h->W * sizeof(u64));
+  if (e == hipSuccess) e = hipMemset(h->cacc, 0, (size_t)E * E * sizeof(uint32_t));
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (e != hipSuccess) {
+    if (h->hist) (void)hipFree(h->hist);
+    if (h->cacc) (void)hipFree(h->cacc);
+    delete h;
+    return hip_status(e, "do_stream_create");
+  }
+  *out = h;
+  return DO_OK;
+}
+
+namespace {
+
+do_status check_handle(const do_stream* h) {
+  if (h == nullptr) return fail(DO_ERR_INVALID_ARG, "stream handle is NULL");
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev != h->device)
+    return fail(DO_ERR_INVALID_ARG, "the handle's device is not the current device");
+  return DO_OK;
+}
+
+do_status stream_append(do_stream* h, const void* const* scores, do_dtype dtype, int64_t n, int32_t count,
+                        hipStream_t stream) {
+  DO_TRY(check_handle(h));
+  DO_TRY(check_dtype(dtype));
+  if (n < 0) return fail(DO_ERR_INVALID_ARG, "n_tokens must be >= 0");
+  if (count < 1 || count > dol::kMaxSeg) return fail(DO_ERR_INVALID_ARG, "count must be in [1, 64]");
+  bool fast = true;
+  for (int i = 0; i < count; ++i) {
+    DO_TRY(check_scores(scores[i], dtype));
+    fast = fast && fast_layout(scores[i], dtype, h->E);
+  }
+  if (n == 0) return DO_OK;
+  if ((h->capacity - h->tokens) / count < n)
+    return fail(DO_ERR_CAPACITY, "append would exceed the history capacity");
+  dol::PathArgs a{};
+  a.E = h->E;
+  a.k = h->k;
+  a.bits = h->hist;
+  a.bits_layer_words = (int64_t)h->E * h->W;
+  a.W = h->W;
+  a.or_partial = 1;
+  a.cacc = h->E <= dol::kFastMaxE ? h->cacc : nullptr;  // wider E: Gram of the whole history at finalize
+  a.cacc_layer_elems = (int64_t)h->E * h->E;
+  dol::SegTable tab{};
+  for (int i = 0; i < count; ++i) {
+    tab.s[i].scores = scores[i];
+    tab.s[i].n = n;
+    tab.s[i].tok_off = h->tokens + (int64_t)i * n;
+    tab.s[i].layer = 0;
+  }
+  DO_TRY(hip_status(profiled(stream, [&] { return dol::launch_topk(dtype, tab, count, n, a, fast, stream); }),
+                    "stream append"));
+  h->tokens += (int64_t)count * n;
+  return DO_OK;
+}
+
+}  // namespace
+
+DOLOSS_API do_status do_stream_append(do_stream* h, const void* scores, do_dtype dtype, int64_t n_tokens,
+                                      hipStream_t stream) {
+  const void* one[1] = {scores};
+  return stream_append(h, one, dtype, n_tokens, 1, stream);
+}
+
+DOLOSS_API do_status do_stream_append_many(do_stream* h, const void* const* scores, do_dtype dtype,
+                                           int64_t n_tokens_each, int32_t count, hipStream_t stream) {
+  if (scores == nullptr) return fail(DO_ERR_INVALID_ARG, "scores pointer array is NULL");
+  if (count < 1 || count > dol::kMaxSeg) return fail(DO_ERR_INVALID_ARG, "count must be in [1, 64]");
+  return stream_append(h, scores, dtype, n_tokens_each, count, stream);
+}
+
+DOLOSS_API do_status do_stream_finalize(do_stream* h, uint32_t* D, do_loss_result* out, hipStream_t stream) {
+  DO_TRY(check_handle(h));
+  if (D == nullptr || !aligned(D, 4)) return fail(DO_ERR_INVALID_ARG, "D is NULL or not 4-byte aligned");
+  if (out == nullptr || !aligned(out, 8)) return fail(DO_ERR_INVALID_ARG, "out is NULL or not 8-byte aligned");
+  if (h->E <= dol::kFastMaxE) return hip_status(dol::launch_finalize(h->cacc, D, out, h->E, 1, stream), "finalize");
+  DO_TRY(hip_status(dol::launch_fill_u32(D, (int64_t)h->E * h->E, 0u, stream), "fill"));
+  DO_TRY(hip_status(dol::launch_gram_bits(h->hist, h->W, h->E, 1, D, stream), "gram"));
+  return hip_status(dol::launch_finalize(D, D, out, h->E, 1, stream), "finalize");
+}
+
+DOLOSS_API do_status do_stream_reset(do_stream* h, hipStream_t stream) {
+  DO_TRY(check_handle(h));
+  DO_TRY(hip_status(dol::launch_fill_u64(h->hist, (int64_t)h->E * h->W, stream), "reset"));
+  DO_TRY(hip_status(dol::launch_fill_u32(h->cacc, (int64_t)h->E * h->E, 0u, stream), "reset"));
+  h->tokens = 0;
+  return DO_OK;
+}
+
+DOLOSS_API do_status do_stream_destroy(do_stream* h) {
+  if (h == nullptr) return DO_OK;
+  hipError_t e = hipDeviceSynchronize();
+  const hipError_t e1 = hipFree(h->hist);
+  const hipError_t e2 = hipFree(h->cacc);
+  delete h;
+  if (e == hipSuccess) e = e1;
+  if (e == hipSuccess) e = e2;
+  return hip_status(e, "do_stream_destroy");
+}
+
+DOLOSS_API const uint64_t* do_stream_bits(const do_stream* h) {
+  return h ? reinterpret_cast<const uint64_t*>(h->hist) : nullptr;
+}
+
+DOLOSS_API int64_t do_stream_tokens(const do_stream* h) { return h ? h->tokens : -1; }
+
+DOLOSS_API int64_t do_stream_words_per_expert(const do_stream* h) { return h ? h->W : -1; }

@@ -1,0 +1,73 @@
+// Internal declarations shared by the kernels and the host dispatch of the
+// DO-loss library.  Not part of the public ABI (see include/doloss.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/doloss.h"
+
+namespace dol {
+
+using u64 = unsigned long long;
+
+constexpr int kWave = 64;
+constexpr int kFusedWaves = 8;                       // waves per block of the Top-K (+Gram) kernel
+constexpr int kFusedThreads = kFusedWaves * kWave;   // 512
+constexpr int kMaxSeg = 64;                          // score segments per launch
+constexpr int kMaxE = 1024;
+constexpr int kFastMaxE = 256;                       // expert index fits the 8 low bits of a composite key
+constexpr int kFastMaxK = 8;                         // width of the in-register Top-K network
+
+// One contiguous block of token rows [n][E] and where its signatures go.
+struct Segment {
+  const void* scores;  // device, [n][E]
+  int64_t n;           // tokens in this segment
+  int64_t tok_off;     // bit position of token 0 in the output signature rows
+  int32_t layer;       // output layer (bits / accumulator / D index)
+  int32_t pad_;
+};
+
+struct SegTable {
+  Segment s[kMaxSeg];
+};
+
+// Where one launch writes its results.
+struct PathArgs {
+  int32_t E;
+  int32_t k;
+  u64* bits;                // nullable: signatures [layer][E][W]
+  int64_t bits_layer_words; // words per layer of `bits`
+  int64_t W;                // words per expert row of `bits`
+  int32_t or_partial;       // words shared with other segments are OR-ed (history), else stored
+  int32_t pad_;
+  uint32_t* cacc;           // nullable: co-occurrence accumulators [layer][E][E], upper triangle
+  int64_t cacc_layer_elems;
+};
+
+struct DevInfo {
+  int device;
+  int cu_count;
+};
+DevInfo device_info();
+
+hipError_t launch_fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s);
+hipError_t launch_fill_u64(u64* p, int64_t n, hipStream_t s);
+
+// Top-K signatures of `nseg` segments; with a.cacc also the co-occurrence
+// counts of each segment's tokens added into a.cacc (popcount Gram).
+hipError_t launch_topk(do_dtype dt, const SegTable& tab, int nseg, int64_t max_seg_tokens, const PathArgs& a,
+                       bool fast_ok, hipStream_t s);
+
+// Co-occurrence counts of existing signatures: cacc[l][i][j] += popcount(F_i & F_j), i <= j.
+hipError_t launch_gram_bits(const u64* bits, int64_t W, int32_t E, int32_t L, uint32_t* cacc, hipStream_t s);
+
+// D = c_ii + c_jj - 2 c_ij (symmetric, zero diagonal); out (nullable) = loss.
+// cacc may alias D.
+hipError_t launch_finalize(const uint32_t* cacc, uint32_t* D, do_loss_result* out, int32_t E, int32_t L,
+                           hipStream_t s);
+
+// Loss of arbitrary distance matrices.
+hipError_t launch_loss(const uint32_t* D, int32_t E, int32_t L, do_loss_result* out, hipStream_t s);
+
+}  // namespace dol

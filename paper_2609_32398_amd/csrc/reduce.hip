@@ -1,0 +1,273 @@
+// Gram of stored signatures, distance finalisation and the loss reduction.
+//
+// Paper: Sec. 3.1.3, Eq. (6) -- G_ij = ||F_i - F_j||_1, evaluated through the
+// identity of App. C.3, ||F_i - F_j||_1 = ||F_i||_1 + ||F_j||_1 - 2 c_ij with
+// c_ij = sum_t f_it f_jt = popcount(F_i AND F_j) and ||F_i||_1 = c_ii.
+// Sec. 3.1.1, Eq. (3) -- L_origin_DO = sum_{i != j} G_ij^2, reported with the
+// mean and the population variance of the off-diagonal G_ij (App. C.1: under
+// the fixed total of Eq. (2), minimising the sum of squares minimises the
+// variance).  All counts and sums are exact integers; only mean, variance and
+// the fp64 copy of the loss are rounded.
+#include <algorithm>
+
+#include "common.h"
+
+namespace dol {
+namespace {
+
+constexpr int kGramThreads = 256;
+constexpr int kGramSlots = 8;   // signature words per expert staged per step
+constexpr int kGramMtq = 4;     // 4x4 micro-tiles per thread
+
+__global__ void k_fill_u32(uint32_t* p, int64_t n, uint32_t v) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = v;
+}
+
+__global__ void k_fill_u64(u64* p, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = 0ull;
+}
+
+// grid = (word-chunk blocks, micro-tile slices, layers).  Each thread owns up
+// to kGramMtq 4x4 micro-tiles of the upper triangle and accumulates
+// popcount(F_i & F_j) over the word chunks of its block in registers.
+__global__ __launch_bounds__(kGramThreads) void k_gram_bits(const u64* __restrict__ bits, int64_t W, int E,
+                                                            uint32_t* __restrict__ cacc) {
+  extern __shared__ __align__(16) u64 tile[];  // [kGramSlots][E4]
+  const int E4 = (E + 3) & ~3;
+  const int NB = E4 / 4;
+  const int NMT = NB * (NB + 1) / 2;
+  const int tid = threadIdx.x;
+  const int layer = blockIdx.z;
+  const u64* lb = bits + (int64_t)layer * E * W;
+
+  int ra[kGramMtq], rb[kGramMtq];
+  uint32_t acc[kGramMtq][16];
+#pragma unroll
+  for (int q = 0; q < kGramMtq; ++q) {
+    int mt = (int)blockIdx.y * kGramThreads * kGramMtq + q * kGramThreads + tid;
+    int a = -1, b = -1;
+    if (mt < NMT) {
+      a = 0;
+      while (mt >= NB - a) {
+        mt -= NB - a;
+        ++a;
+      }
+      b = a + mt;
+    }
+    ra[q] = a;
+    rb[q] = b;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc[q][i] = 0;
+  }
+
+  const int64_t nchunks = (W + kGramSlots - 1) / kGramSlots;
+  for (int64_t ch = blockIdx.x; ch < nchunks; ch += gridDim.x) {
+    const int64_t w0 = ch * kGramSlots;
+    __syncthreads();
+    for (int f = tid; f < E4 * kGramSlots; f += kGramThreads) {
+      const int e = f / kGramSlots, s = f % kGramSlots;
+      u64 v = 0;
+      if (e < E && w0 + s < W) v = lb[(int64_t)e * W + w0 + s];
+      tile[s * E4 + e] = v;
+    }
+    __syncthreads();
+    for (int s = 0; s < kGramSlots; ++s) {
+      const u64* w = tile + s * E4;
+#pragma unroll
+      for (int q = 0; q < kGramMtq; ++q) {
+        if (ra[q] < 0) continue;
+        const ulonglong2 a01 = *reinterpret_cast<const ulonglong2*>(w + 4 * ra[q]);
+        const ulonglong2 a23 = *reinterpret_cast<const ulonglong2*>(w + 4 * ra[q] + 2);
+        const ulonglong2 b01 = *reinterpret_cast<const ulonglong2*>(w + 4 * rb[q]);
+        const ulonglong2 b23 = *reinterpret_cast<const ulonglong2*>(w + 4 * rb[q] + 2);
+        const u64 A[4] = {a01.x, a01.y, a23.x, a23.y};
+        const u64 B[4] = {b01.x, b01.y, b23.x, b23.y};
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) acc[q][i * 4 + j] += (uint32_t)__popcll(A[i] & B[j]);
+      }
+    }
+  }
+  uint32_t* c = cacc + (int64_t)layer * E * E;
+#pragma unroll
+  for (int q = 0; q < kGramMtq; ++q) {
+    if (ra[q] < 0) continue;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int gi = 4 * ra[q] + i, gj = 4 * rb[q] + j;
+        const uint32_t v = acc[q][i * 4 + j];
+        if (gi <= gj && gj < E && v) atomicAdd(&c[(int64_t)gi * E + gj], v);
+      }
+  }
+}
+
+// 64 x 64 -> 128-bit product as (hi, lo).
+__device__ __forceinline__ void mul128(u64 a, u64 b, u64& hi, u64& lo) {
+  lo = a * b;
+  hi = __umul64hi(a, b);
+}
+
+// Fill one loss record from exact sums over the E(E-1) off-diagonal entries.
+__device__ void write_result(do_loss_result* o, u64 s1, u64 s2, int E) {
+  if (E < 2) {
+    o->sum = 0;
+    o->sumsq = 0;
+    o->loss = 0.0;
+    o->mean = 0.0;
+    o->var = 0.0;
+    return;
+  }
+  const u64 P = (u64)E * (u64)(E - 1);
+  o->sum = s1;
+  o->sumsq = s2;
+  o->loss = (double)s2;
+  o->mean = (double)s1 / (double)P;
+  // population variance = (P*s2 - s1^2) / P^2 with an exact 128-bit numerator
+  u64 ah, al, bh, bl;
+  mul128(P, s2, ah, al);
+  mul128(s1, s1, bh, bl);
+  const u64 nl = al - bl;
+  const u64 nh = ah - bh - (al < bl ? 1ull : 0ull);
+  const double num = (double)nh * 18446744073709551616.0 + (double)nl;
+  o->var = num / ((double)P * (double)P);
+}
+
+__device__ __forceinline__ u64 wave_sum(u64 v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+// Sum (s1, s2) across the block; valid in thread 0.
+__device__ void block_sum2(u64& s1, u64& s2) {
+  __shared__ u64 part[2][16];
+  s1 = wave_sum(s1);
+  s2 = wave_sum(s2);
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int nw = (blockDim.x + 63) >> 6;
+  if (lane == 0) {
+    part[0][wave] = s1;
+    part[1][wave] = s2;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    u64 a = 0, b = 0;
+    for (int i = 0; i < nw; ++i) {
+      a += part[0][i];
+      b += part[1][i];
+    }
+    s1 = a;
+    s2 = b;
+  }
+}
+
+// One block per layer.  cacc may alias D: the diagonal is read before any
+// write, and every other element is read and written only by the thread that
+// owns its (i < j) pair.
+__global__ __launch_bounds__(1024) void k_finalize(const uint32_t* cacc, uint32_t* D, do_loss_result* out, int E) {
+  __shared__ uint32_t diag[kMaxE];
+  const int64_t EE = (int64_t)E * E;
+  const uint32_t* c = cacc + blockIdx.x * EE;
+  uint32_t* d = D + blockIdx.x * EE;
+  for (int i = threadIdx.x; i < E; i += blockDim.x) diag[i] = c[(int64_t)i * E + i];
+  __syncthreads();
+  u64 s1 = 0, s2 = 0;
+  for (int64_t p = threadIdx.x; p < EE; p += blockDim.x) {
+    const int i = (int)(p / E), j = (int)(p % E);
+    if (i < j) {
+      const uint32_t v = diag[i] + diag[j] - 2u * c[p];
+      d[p] = v;
+      d[(int64_t)j * E + i] = v;
+      s1 += 2ull * v;
+      s2 += 2ull * (u64)v * (u64)v;
+    } else if (i == j) {
+      d[p] = 0u;
+    }
+  }
+  if (out == nullptr) return;
+  block_sum2(s1, s2);
+  if (threadIdx.x == 0) write_result(out + blockIdx.x, s1, s2, E);
+}
+
+__global__ __launch_bounds__(1024) void k_loss(const uint32_t* D, do_loss_result* out, int E) {
+  const int64_t EE = (int64_t)E * E;
+  const uint32_t* d = D + blockIdx.x * EE;
+  u64 s1 = 0, s2 = 0;
+  for (int64_t p = threadIdx.x; p < EE; p += blockDim.x) {
+    const int i = (int)(p / E), j = (int)(p % E);
+    if (i != j) {
+      const u64 v = d[p];
+      s1 += v;
+      s2 += v * v;
+    }
+  }
+  block_sum2(s1, s2);
+  if (threadIdx.x == 0) write_result(out + blockIdx.x, s1, s2, E);
+}
+
+}  // namespace
+
+DevInfo device_info() {
+  static thread_local int cached_dev = -1;
+  static thread_local int cached_cu = 0;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) dev = 0;
+  if (dev != cached_dev) {
+    int cu = 0;
+    if (hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cu < 1) cu = 1;
+    cached_dev = dev;
+    cached_cu = cu;
+  }
+  return DevInfo{cached_dev, cached_cu};
+}
+
+hipError_t launch_fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const int64_t blocks = std::min<int64_t>((n + 255) / 256, 4096);
+  hipLaunchKernelGGL(k_fill_u32, dim3((unsigned)blocks), dim3(256), 0, s, p, n, v);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_u64(u64* p, int64_t n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const int64_t blocks = std::min<int64_t>((n + 255) / 256, 4096);
+  hipLaunchKernelGGL(k_fill_u64, dim3((unsigned)blocks), dim3(256), 0, s, p, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_gram_bits(const u64* bits, int64_t W, int32_t E, int32_t L, uint32_t* cacc, hipStream_t s) {
+  const int E4 = (E + 3) & ~3;
+  const int NB = E4 / 4;
+  const int NMT = NB * (NB + 1) / 2;
+  const int per_slice = kGramThreads * kGramMtq;
+  const int slices = (NMT + per_slice - 1) / per_slice;
+  const size_t lds = (size_t)kGramSlots * E4 * sizeof(u64);
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k_gram_bits),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  const int64_t nchunks = (W + kGramSlots - 1) / kGramSlots;
+  const DevInfo di = device_info();
+  int64_t bx = ((int64_t)di.cu_count * 4 + (int64_t)slices * L - 1) / ((int64_t)slices * L);
+  bx = std::max<int64_t>(1, std::min<int64_t>(bx, nchunks));
+  hipLaunchKernelGGL(k_gram_bits, dim3((unsigned)bx, (unsigned)slices, (unsigned)L), dim3(kGramThreads), lds, s,
+                     bits, W, E, cacc);
+  return hipGetLastError();
+}
+
+hipError_t launch_finalize(const uint32_t* cacc, uint32_t* D, do_loss_result* out, int32_t E, int32_t L,
+                           hipStream_t s) {
+  hipLaunchKernelGGL(k_finalize, dim3((unsigned)L), dim3(1024), 0, s, cacc, D, out, E);
+  return hipGetLastError();
+}
+
+hipError_t launch_loss(const uint32_t* D, int32_t E, int32_t L, do_loss_result* out, hipStream_t s) {
+  hipLaunchKernelGGL(k_loss, dim3((unsigned)L), dim3(1024), 0, s, D, out, E);
+  return hipGetLastError();
+}
+
+}  // namespace dol

@@ -1,0 +1,118 @@
+"""The C ABI library: it loads, exports every declared symbol, and rejects bad
+arguments on the host before any GPU work (these calls never reach the GPU).
+"""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "doloss.h")
+
+
+@pytest.fixture(scope="module")
+def dl():
+    import paper_2609_32398_amd as p
+
+    if not os.path.exists(p.LIB_PATH):
+        p.build()
+    return p
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(do_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_header_declares_the_path(dl):
+    names = _declared()
+    for must in ("do_topk_signature", "do_pairwise_hamming", "do_loss", "do_fused", "do_stream_create",
+                 "do_stream_append", "do_stream_append_many", "do_stream_finalize"):
+        assert must in names
+
+
+def test_library_exports_every_declared_symbol(dl):
+    out = subprocess.run(["nm", "-D", "--defined-only", dl.LIB_PATH], capture_output=True, text=True, check=True).stdout
+    exported = {l.split()[-1] for l in out.splitlines() if " T " in l}
+    missing = [n for n in _declared() if n not in exported]
+    assert not missing, f"declared but not exported: {missing}"
+    # nothing else leaks out of the library besides the declared API
+    extra = sorted(n for n in exported if n.startswith("do_") and n not in _declared())
+    assert not extra
+
+
+def test_status_strings_and_version(dl):
+    L = dl.lib()
+    assert L.do_status_string(0) == b"DO_OK"
+    assert L.do_status_string(3) == b"DO_ERR_CAPACITY"
+    assert L.do_version() >= 100
+
+
+def _st(dl, fn, *args):
+    return getattr(dl.lib(), fn)(*args)
+
+
+FAKE = 0x10000  # a 64 KiB-aligned non-null address: validation fails before it is ever dereferenced
+
+
+@pytest.mark.parametrize("args,expect", [
+    ((FAKE, 7, 64, 8, 2, 1, FAKE, None), 2),            # bad dtype
+    ((None, 0, 64, 8, 2, 1, FAKE, None), 1),            # NULL scores
+    ((FAKE, 0, 64, 8, 0, 1, FAKE, None), 1),            # k = 0
+    ((FAKE, 0, 64, 8, 9, 1, FAKE, None), 1),            # k > E
+    ((FAKE, 0, 0, 8, 2, 1, FAKE, None), 1),             # N = 0
+    ((FAKE, 0, 64, 0, 1, 1, FAKE, None), 1),            # E = 0
+    ((FAKE, 0, 64, 1025, 2, 1, FAKE, None), 1),         # E too large
+    ((FAKE, 0, 64, 8, 2, 0, FAKE, None), 1),            # L = 0
+    ((FAKE, 0, 1 << 32, 8, 2, 1, FAKE, None), 4),       # N >= 2^32
+    ((FAKE, 0, 64, 8, 2, 1, None, None), 1),            # NULL bits
+    ((FAKE, 0, 64, 8, 2, 1, FAKE + 4, None), 1),        # misaligned bits
+    ((FAKE + 2, 0, 64, 8, 2, 1, FAKE, None), 1),        # fp32 scores not 4-byte aligned
+])
+def test_topk_signature_rejects(dl, args, expect):
+    assert _st(dl, "do_topk_signature", *args) == expect
+    assert dl.lib().do_last_error()
+
+
+def test_overflow_of_exact_sum_of_squares_is_rejected(dl):
+    # E(E-1)N^2 >= 2^64 with N < 2^32: E = 1024, N = 2^27
+    assert _st(dl, "do_fused", FAKE, 0, 1 << 27, 1024, 8, 1, FAKE, FAKE, FAKE, None) == 4
+
+
+def test_fused_rejects(dl):
+    assert _st(dl, "do_fused", FAKE, 0, 64, 8, 2, 1, None, None, FAKE, None) == 1          # NULL D
+    assert _st(dl, "do_fused", FAKE, 0, 64, 8, 2, 1, None, FAKE, None, None) == 1          # NULL out
+    assert _st(dl, "do_fused", FAKE, 0, 64, 300, 2, 1, None, FAKE, FAKE, None) == 1        # E > 256 needs bits
+    assert _st(dl, "do_fused", FAKE, 1, 64, 8, 2, 1, FAKE + 1, FAKE, FAKE, None) == 1      # misaligned bits
+
+
+def test_hamming_and_loss_reject(dl):
+    assert _st(dl, "do_pairwise_hamming", None, 64, 8, 1, FAKE, None) == 1
+    assert _st(dl, "do_pairwise_hamming", FAKE, 64, 8, 1, None, None) == 1
+    assert _st(dl, "do_pairwise_hamming", FAKE, 64, 8, 1, FAKE + 2, None) == 1
+    assert _st(dl, "do_loss", None, 8, 1, FAKE, None) == 1
+    assert _st(dl, "do_loss", FAKE, 8, 1, None, None) == 1
+    assert _st(dl, "do_loss", FAKE, 0, 1, FAKE, None) == 1
+
+
+def test_stream_rejects_without_touching_the_device(dl):
+    L = dl.lib()
+    h = ctypes.c_void_p()
+    assert L.do_stream_create(8, 2, 1000, None) == 1
+    assert L.do_stream_create(8, 9, 1000, ctypes.byref(h)) == 1
+    assert L.do_stream_create(8, 2, 0, ctypes.byref(h)) == 1
+    assert L.do_stream_append(None, FAKE, 0, 10, None) == 1
+    assert L.do_stream_finalize(None, FAKE, FAKE, None) == 1
+    assert L.do_stream_reset(None, None) == 1
+    assert L.do_stream_destroy(None) == 0
+    assert L.do_stream_tokens(None) == -1
+
+
+def test_binding_requires_device_tensors(dl):
+    import torch
+
+    with pytest.raises(ValueError):
+        dl.do_topk_signature(torch.zeros(4, 8), 2)

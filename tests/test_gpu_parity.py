@@ -1,0 +1,272 @@
+"""HIP path vs the CPU oracle, element by element, through the C ABI.
+
+Bar: signatures and distances bit-exact; loss sums exact, the fp64 loss,
+mean and variance within 1e-5 relative of the oracle (spec tolerance).
+"""
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import D_np, bits_np, loss_close, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dl():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_32398_amd as p
+
+    p.lib()
+    return p
+
+
+def _check_layer(dl, orc, scores_np, k, bits, D, rec, label=""):
+    F = orc.topk_signature(scores_np, k)
+    ref_bits = orc.pack(F)
+    ref_D = orc.hamming(F)
+    ref_L = orc.loss(ref_D)
+    if bits is not None:
+        got = bits_np(bits)
+        if not np.array_equal(got, ref_bits):
+            bad = np.argwhere(got != ref_bits)
+            raise AssertionError(f"{label}: {len(bad)} signature words differ, first {bad[:4].tolist()}")
+    np.testing.assert_array_equal(D_np(D), ref_D, err_msg=label)
+    loss_close(rec, ref_L)
+
+
+def _run_all_entry_points(dl, orc, x, k, label):
+    """do_topk_signature, do_pairwise_hamming, do_loss and do_fused on one layer."""
+    print(f"[case] {label} shape={x.shape} dtype={x.dtype} k={k}", flush=True)
+    xd = to_dev(x)
+    N, E = x.shape
+    bits = dl.do_topk_signature(xd, k)
+    D = dl.do_pairwise_hamming(bits, N)
+    out = dl.do_loss(D)
+    torch.cuda.synchronize()
+    _check_layer(dl, orc, x, k, bits[0], D[0], dl.loss_records(out)[0], label + " (separate)")
+    fb, fD, fout = dl.do_fused(xd, k, want_bits=True)
+    torch.cuda.synchronize()
+    _check_layer(dl, orc, x, k, fb[0], fD[0], dl.loss_records(fout)[0], label + " (fused)")
+    _, fD2, fout2 = dl.do_fused(xd, k, want_bits=False)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(D_np(fD2), D_np(fD))
+    assert dl.loss_records(fout2) == dl.loss_records(fout)
+
+
+# ---------------------------------------------------------------------------
+# the small workloads at full size
+# ---------------------------------------------------------------------------
+def test_workload0_e8_k2_n4096_f32(dl, orc, syn):
+    x = syn.workload_fill(0, 0)
+    _run_all_entry_points(dl, orc, x, 2, "workload0")
+
+
+def test_workload1_e64_k6_n65536_bf16(dl, orc, syn):
+    x = syn.workload_fill(1, 0)
+    _run_all_entry_points(dl, orc, x, 6, "workload1")
+
+
+# ---------------------------------------------------------------------------
+# shapes, ties and special values
+# ---------------------------------------------------------------------------
+SHAPES = [
+    (1, 1, 1), (3, 1, 5), (3, 3, 64), (5, 2, 63), (8, 8, 65), (13, 4, 100), (16, 1, 129), (24, 7, 1000),
+    (37, 8, 257), (64, 8, 4097), (100, 3, 333), (128, 8, 3000), (200, 5, 1234), (256, 8, 2500), (256, 1, 700),
+]
+
+
+@pytest.mark.parametrize("E,k,N", SHAPES)
+@pytest.mark.parametrize("dtype", [0, 1])
+def test_random_shapes_normal(dl, orc, syn, E, k, N, dtype):
+    x = syn.normal(1000 + 7 * E + N, N, E, dtype)
+    _run_all_entry_points(dl, orc, x, k, f"normal E={E} k={k} N={N}")
+
+
+@pytest.mark.parametrize("E,k,N", [(8, 2, 500), (24, 8, 700), (64, 6, 999), (128, 8, 1500), (256, 8, 640),
+                                   (40, 3, 128), (96, 8, 200)])
+@pytest.mark.parametrize("dtype", [0, 1])
+def test_tie_heavy_integer_scores(dl, orc, syn, E, k, N, dtype):
+    x = syn.int_ties(77 + E, N, E, -3, 3, dtype)
+    _run_all_entry_points(dl, orc, x, k, f"ties E={E} k={k} N={N}")
+
+
+@pytest.mark.parametrize("E,k,N", [(12, 9, 300), (64, 20, 200), (33, 33, 100), (300, 8, 150), (1024, 12, 70),
+                                   (520, 1, 90)])
+def test_slow_paths_large_k_and_wide_E(dl, orc, syn, E, k, N):
+    x = syn.normal(5 + E, N, E, 0)
+    print(f"[case] slow E={E} k={k} N={N}", flush=True)
+    xd = to_dev(x)
+    bits = dl.do_topk_signature(xd, k)
+    D = dl.do_pairwise_hamming(bits, N)
+    out = dl.do_loss(D)
+    fb, fD, fout = dl.do_fused(xd, k, want_bits=True)
+    torch.cuda.synchronize()
+    _check_layer(dl, orc, x, k, bits[0], D[0], dl.loss_records(out)[0], "slow separate")
+    _check_layer(dl, orc, x, k, fb[0], fD[0], dl.loss_records(fout)[0], "slow fused")
+
+
+def _special_rows(dtype, E, N, seed):
+    rng = np.random.default_rng(seed)
+    vals32 = np.array([0.0, -0.0, np.inf, -np.inf, np.nan, 1.0, -1.0, 1e-40, -1e-40, 3.5], dtype=np.float32)
+    x = rng.standard_normal((N, E)).astype(np.float32)
+    mask = rng.random((N, E)) < 0.3
+    x[mask] = rng.choice(vals32, size=mask.sum())
+    x[0, :] = -0.0
+    x[1, :] = np.nan
+    x[2, ::2] = np.inf
+    x[3, :] = 0.0
+    x[3, ::3] = -0.0
+    x[4, :] = -np.inf
+    x[4, 1] = np.nan
+    if dtype == 0:
+        return x
+    b = x.view(np.uint32)
+    return (b >> 16).astype(np.uint16)  # truncation keeps every special value (and makes more ties)
+
+
+@pytest.mark.parametrize("E,k,N", [(8, 2, 300), (16, 8, 200), (64, 6, 256), (256, 8, 128), (40, 5, 100)])
+@pytest.mark.parametrize("dtype", [0, 1])
+def test_special_values(dl, orc, E, k, N, dtype):
+    x = _special_rows(dtype, E, N, E * 31 + k)
+    _run_all_entry_points(dl, orc, x, k, f"specials E={E} k={k}")
+
+
+@pytest.mark.parametrize("dtype", [0, 1])
+def test_negative_and_bucket_ties_fp32(dl, orc, syn, dtype):
+    # all-negative scores (threshold below zero) and fp32 values that share
+    # their top 24 bits (force the exact re-rank)
+    x = syn.normal(9, 2000, 64, dtype, mean=-20.0)
+    _run_all_entry_points(dl, orc, x, 8, "negative")
+    if dtype == 0:
+        base = syn.normal(10, 1000, 32, 0)
+        bits = base.view(np.uint32) & np.uint32(0xFFFFFF00)
+        bits = bits | (np.arange(32, dtype=np.uint32)[None, ::-1] & np.uint32(0xFF))
+        _run_all_entry_points(dl, orc, bits.view(np.float32), 5, "bucket ties")
+
+
+def test_misaligned_scores_take_the_exact_path(dl, orc, syn):
+    N, E, k = 500, 64, 6
+    x = syn.normal(3, N, E, 0)
+    buf = torch.zeros(N * E + 1, dtype=torch.float32, device="cuda")
+    buf[1:] = torch.from_numpy(x.reshape(-1)).cuda()
+    xd = buf[1:].view(N, E)
+    assert xd.data_ptr() % 16 != 0
+    bits = dl.do_topk_signature(xd, k)
+    _, D, out = dl.do_fused(xd, k)
+    torch.cuda.synchronize()
+    _check_layer(dl, orc, x, k, bits[0], D[0], dl.loss_records(out)[0], "misaligned")
+
+
+def test_multi_layer_batching_beyond_one_launch(dl, orc, syn):
+    L, N, E, k = 70, 130, 16, 3
+    x = np.stack([syn.normal(40 + l, N, E, 1) for l in range(L)])
+    xd = to_dev(x.reshape(L * N, E)).view(L, N, E)
+    fb, fD, fout = dl.do_fused(xd, k, want_bits=True)
+    bits = dl.do_topk_signature(xd, k)
+    torch.cuda.synchronize()
+    recs = dl.loss_records(fout)
+    for l in (0, 1, 63, 64, 69):
+        _check_layer(dl, orc, x[l], k, fb[l], fD[l], recs[l], f"layer {l}")
+    np.testing.assert_array_equal(bits_np(bits), bits_np(fb))
+
+
+def test_loss_of_arbitrary_matrices(dl):
+    rng = np.random.default_rng(0)
+    for E in (1, 2, 7, 300):
+        D = rng.integers(0, 1 << 20, size=(3, E, E), dtype=np.uint32)
+        out = dl.do_loss(torch.from_numpy(D.view(np.int32)).cuda())
+        torch.cuda.synchronize()
+        recs = dl.loss_records(out)
+        for l in range(3):
+            off = ~np.eye(E, dtype=bool)
+            v = D[l][off].astype(object)
+            s1 = int(sum(v)) if E > 1 else 0
+            s2 = int(sum(a * a for a in v)) if E > 1 else 0
+            P = E * (E - 1)
+            assert recs[l]["sum"] == s1 and recs[l]["sumsq"] == s2
+            if E > 1:
+                assert recs[l]["mean"] == pytest.approx(s1 / P, rel=1e-12)
+                assert recs[l]["var"] == pytest.approx((s2 * P - s1 * s1) / (P * P), rel=1e-9)
+            else:
+                assert recs[l] == dict(sum=0, sumsq=0, loss=0.0, mean=0.0, var=0.0)
+
+
+def test_hamming_of_oracle_signatures(dl, orc, syn):
+    x = syn.normal(12, 5000, 96, 1)
+    F = orc.topk_signature(x, 7)
+    words = orc.pack(F)
+    D = dl.do_pairwise_hamming(torch.from_numpy(words.view(np.int64)).cuda(), 5000)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(D_np(D)[0], orc.hamming(F))
+
+
+def test_determinism_bit_identical_reruns(dl, syn):
+    x = to_dev(syn.normal(2, 20000, 128, 1))
+    a = dl.do_fused(x, 8, want_bits=True)
+    b = dl.do_fused(x, 8, want_bits=True)
+    torch.cuda.synchronize()
+    assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1]) and torch.equal(a[2], b[2])
+
+
+# ---------------------------------------------------------------------------
+# streaming history
+# ---------------------------------------------------------------------------
+def test_stream_unaligned_appends_equal_one_batch(dl, orc, syn):
+    E, k = 64, 6
+    sizes = [1000, 37, 64, 1, 4096, 130, 63]
+    parts = [syn.normal(500 + i, n, E, 1) for i, n in enumerate(sizes)]
+    s = dl.DoStream(E, k, 10000)
+    for p in parts:
+        s.append(to_dev(p))
+    assert s.tokens == sum(sizes)
+    D, out = s.finalize()
+    torch.cuda.synchronize()
+    F, words, ref_D, ref_L = orc.run_stream(parts, k)
+    np.testing.assert_array_equal(D_np(D), ref_D)
+    loss_close(dl.loss_records(out)[0], ref_L)
+    hist = s.history()
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(bits_np(hist)[:, : words.shape[1]], words)
+    assert not bits_np(hist)[:, words.shape[1]:].any()
+    # finalize twice gives the same answer; reset clears everything
+    D2, out2 = s.finalize()
+    torch.cuda.synchronize()
+    assert torch.equal(D, D2)
+    s.reset()
+    D3, out3 = s.finalize()
+    torch.cuda.synchronize()
+    assert s.tokens == 0 and int(D3.abs().sum()) == 0
+    s.close()
+
+
+def test_stream_append_many_and_capacity(dl, orc, syn):
+    E, k, nmb = 128, 8, 5
+    parts = [syn.normal(900 + i, 777, E, 1) for i in range(nmb)]
+    s = dl.DoStream(E, k, 777 * nmb)
+    s.append_many([to_dev(p) for p in parts])
+    D, out = s.finalize()
+    torch.cuda.synchronize()
+    F, words, ref_D, ref_L = orc.run_stream(parts, k)
+    np.testing.assert_array_equal(D_np(D), ref_D)
+    loss_close(dl.loss_records(out)[0], ref_L)
+    with pytest.raises(dl.DoLossError) as ei:
+        s.append(to_dev(parts[0][:1]))
+    assert ei.value.status == dl.DO_ERR_CAPACITY
+    assert s.tokens == 777 * nmb
+    s.close()
+
+
+def test_stream_wide_E_gram_at_finalize(dl, orc, syn):
+    E, k = 300, 4
+    parts = [syn.normal(60 + i, n, E, 0) for i, n in enumerate([100, 65, 300])]
+    s = dl.DoStream(E, k, 465)
+    for p in parts:
+        s.append(to_dev(p))
+    D, out = s.finalize()
+    torch.cuda.synchronize()
+    F, words, ref_D, ref_L = orc.run_stream(parts, k)
+    np.testing.assert_array_equal(D_np(D), ref_D)
+    loss_close(dl.loss_records(out)[0], ref_L)
+    s.close()
