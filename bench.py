@@ -37,6 +37,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-tokens", type=int, default=1 << 20)
     ap.add_argument("--layers", type=int, default=None, help="override the layer count (testing only)")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a plain 4 GiB device copy (calibrates the HBM byte counters)")
     return ap.parse_args()
 
 
@@ -252,6 +254,15 @@ def main():
     import paper_2609_32398_amd as dl
 
     dl.lib()
+    if args.calibrate_copy:
+        n = 1 << 30  # 4 GiB of fp32
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps(dict(calibration="device copy", bytes_read=4 * n, bytes_written=4 * n, launches=3)))
+        return
     cfg = args.workload
     res = bench_stream(args) if cfg == 3 else bench_layers(args, cfg)
     if not args.no_cpu_baseline:

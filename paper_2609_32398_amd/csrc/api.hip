@@ -106,7 +106,7 @@ do_status run_layers(const void* scores, do_dtype dt, int64_t N, int32_t E, int3
       tab.s[i].tok_off = 0;
       tab.s[i].layer = l0 + i;
     }
-    DO_TRY(hip_status(profiled(s, [&] { return dol::launch_topk(dt, tab, nseg, N, a, fast, s); }), "top-k launch"));
+    DO_TRY(hip_status(profiled(s, [&] { return dol::launch_topk(dt, tab, nseg, a, fast, s); }), "top-k launch"));
   }
   return DO_OK;
 }
@@ -263,7 +263,7 @@ do_status stream_append(do_stream* h, const void* const* scores, do_dtype dtype,
     tab.s[i].tok_off = h->tokens + (int64_t)i * n;
     tab.s[i].layer = 0;
   }
-  DO_TRY(hip_status(profiled(stream, [&] { return dol::launch_topk(dtype, tab, count, n, a, fast, stream); }),
+  DO_TRY(hip_status(profiled(stream, [&] { return dol::launch_topk(dtype, tab, count, a, fast, stream); }),
                     "stream append"));
   h->tokens += (int64_t)count * n;
   return DO_OK;

@@ -28,8 +28,14 @@ struct Segment {
   int32_t pad_;
 };
 
+// Segments of one launch.  tile_start[i] is the number of 64-position
+// signature words of segments 0..i-1 (filled by launch_topk): the blocks of a
+// launch split the concatenated word range [0, tile_start[nseg]) evenly.
 struct SegTable {
   Segment s[kMaxSeg];
+  int64_t tile_start[kMaxSeg + 1];
+  int32_t nseg;
+  int32_t pad_;
 };
 
 // Where one launch writes its results.
@@ -56,8 +62,7 @@ hipError_t launch_fill_u64(u64* p, int64_t n, hipStream_t s);
 
 // Top-K signatures of `nseg` segments; with a.cacc also the co-occurrence
 // counts of each segment's tokens added into a.cacc (popcount Gram).
-hipError_t launch_topk(do_dtype dt, const SegTable& tab, int nseg, int64_t max_seg_tokens, const PathArgs& a,
-                       bool fast_ok, hipStream_t s);
+hipError_t launch_topk(do_dtype dt, SegTable& tab, int nseg, const PathArgs& a, bool fast_ok, hipStream_t s);
 
 // Co-occurrence counts of existing signatures: cacc[l][i][j] += popcount(F_i & F_j), i <= j.
 hipError_t launch_gram_bits(const u64* bits, int64_t W, int32_t E, int32_t L, uint32_t* cacc, hipStream_t s);

@@ -1,59 +1,84 @@
-// Router Top-K, signature packing and (optionally) the co-occurrence Gram of
-// the DO-loss path, in one pass over the scores.
+// Router Top-K, signature packing and the co-occurrence Gram of the DO-loss
+// path, in one pass over the scores.
 //
 // Paper: Sec. 3.1.1, Eq. (1) -- f_it = 1 iff expert i is in the Top-K of
 // token t; the binary load signature F_i collects f_it over the batch.
 // Sec. 3.1.3, Eq. (6) and App. C.3 -- ||F_i - F_j||_1 = c_ii + c_jj - 2 c_ij
 // with c_ij = sum_t f_it f_jt, which is what the Gram part accumulates.
 //
-// Layout of the work: one wavefront owns 64 consecutive output bit positions
-// (one signature word per expert); lane l ranks token (64*w + l - tok_off).
-// Score rows are streamed through LDS in 128-byte column chunks so that the
-// global loads are fully coalesced, then every lane reads its own row back.
+// Work layout.  A block of 8 wavefronts owns 8 consecutive signature words
+// (512 output bit positions) per step; lane l of wave w ranks token
+// 64*(word) + l - tok_off.  Score rows stream through LDS in 128-byte column
+// chunks so the global loads are fully coalesced; the next chunk's loads are
+// issued before the current chunk is ranked, so each wave keeps one chunk in
+// flight at all times.  The 8 signature words of a step land in an LDS tile
+// (double-buffered) from which the block writes them out as 64-byte runs and
+// feeds the Gram.
 //
-// Exact Top-K with a composite 32-bit key per element: the score's bits are
-// mapped to an order-preserving signed integer, the low byte (fp32) or the
-// low half (bf16) is replaced by (255 - expert index), so larger keys rank
-// first and equal values fall to the lower index.  bf16 keeps its full 16-bit
-// value, so the key order is exact; fp32 keeps the top 24 bits, so a token is
-// re-ranked exactly when the k-th and (k+1)-th keys share a 24-bit bucket.
-// Signed zeros, infinities and NaN near the threshold also send the token to
-// the exact per-lane fallback (64-bit keys, k selection passes).
+// Exact Top-K with composite 32-bit keys.  Each element becomes one signed
+// integer whose high bits order the score and whose low byte is (255 - expert
+// index), so larger keys rank first and equal scores fall to the lower index.
+// "Positive" keys use the raw bit pattern (one instruction, exact whenever the
+// k-th score is a positive number); "general" keys first map the pattern to
+// an order-preserving integer (exact for all non-NaN values except that -0
+// sorts one step below +0).  bf16 keeps all 16 value bits; fp32 keeps 24, so
+// a token is re-ranked exactly when its k-th and (k+1)-th keys share a 24-bit
+// bucket.  Any token whose threshold lands on +-0, +-inf, NaN or a bucket tie,
+// or whose threshold is not positive under positive keys, is re-ranked by an
+// exact per-lane fallback on 64-bit keys.  bf16 always uses general keys (they
+// cost it little); an fp32 wave starts with positive keys and switches to
+// general keys for the rest of its tiles after meeting a non-positive threshold.
+//
+// Gram.  mode 2 (default): int8 MFMA 32x32x32 on 0/1 bytes expanded from the
+// signature words, one or more 32x32 expert tile pairs per wave, accumulators
+// in registers for the whole kernel.  mode 1: VALU popcount(a & b) on 4x4
+// micro-tiles per thread.  Either way each block adds its integer partial
+// counts into the accumulator matrix once at the end (order-independent).
+#include <cstdlib>
+
 #include "common.h"
 
 namespace dol {
 namespace {
 
 typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v16i __attribute__((ext_vector_type(16)));
+typedef short v2s __attribute__((ext_vector_type(2)));
 
-constexpr int kStageStride = 144;  // bytes per staged row: 8 x 16-byte vectors + 16 bytes of padding
+// Per wave, two 8 KiB stage buffers of 64 rows x 128 bytes.  Piece q of row r
+// lives at slot q ^ swz(r), swz(r) = (r & 7) ^ ((r >> 3) & 1): the per-lane row
+// reads are then bank-conflict free and each direct-to-LDS load instruction
+// still reads whole 128-byte row segments.
+constexpr int kChunkBytes = 64 * 128;
+constexpr int kStageBytes = kFusedWaves * 2 * kChunkBytes;
+
+__device__ __forceinline__ int row_swizzle(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+
+// s_waitcnt vmcnt(0) (expcnt and lgkmcnt left at their maxima)
+#define DOL_WAIT_VMEM() __builtin_amdgcn_s_waitcnt(0x0F70)
+
+constexpr int kGramNone = 0, kGramPopc = 1, kGramMfma = 2;
+
+constexpr int kCompPosInf = 0x7F800000;          // key >= this: +inf or NaN
+constexpr int kCompNegInfMax = (int)0x807FFFFF;  // general key <= this: -inf or NaN
 
 template <typename T>
 struct Traits;
 template <>
 struct Traits<float> {
-  static constexpr int kVec = 4;                    // elements per 16-byte vector
-  static constexpr uint32_t kHiMask = 0xFFFFFF00u;  // kept value bits of a composite key
-  static constexpr bool kExact = false;
-  static constexpr int kZeroLo = -256, kZeroHi = 255;  // composite keys of the -0 / +0 buckets
+  static constexpr int kVec = 4;                       // elements per 16-byte vector
+  static constexpr bool kExact = false;                // 24 value bits kept
+  static constexpr int kPosMin = 0x100;                // positive keys: threshold must be >= this
+  static constexpr int kZeroLo = -256, kZeroHi = 255;  // general keys of the -0 / +0 buckets
 };
 template <>
 struct Traits<uint16_t> {
   static constexpr int kVec = 8;
-  static constexpr uint32_t kHiMask = 0xFFFF0000u;
   static constexpr bool kExact = true;
+  static constexpr int kPosMin = 0x10000;
   static constexpr int kZeroLo = -65536, kZeroHi = 65535;
 };
-
-constexpr int kCompPosInf = 0x7F800000;        // composite >= this: +inf or NaN
-constexpr int kCompNegInfMax = (int)0x807FFFFF; // composite <= this: -inf or NaN
-
-// u: fp32 bit pattern (bf16 widened by << 16).  Order-preserving for all
-// non-NaN values except that -0 sorts one step below +0.
-__device__ __forceinline__ int composite(uint32_t u, uint32_t himask, int e) {
-  const uint32_t m = (uint32_t)((int32_t)u >> 31) & 0x7FFFFFFFu;
-  return (int)(((u ^ m) & himask) | (uint32_t)(255 - e));
-}
 
 #define DOL_CAS(a, b)          \
   {                            \
@@ -73,21 +98,81 @@ __device__ __forceinline__ void sort8_desc(int (&g)[8]) {
   DOL_CAS(g[1], g[2]) DOL_CAS(g[3], g[4]) DOL_CAS(g[5], g[6])
 }
 
-// top <- the 8 largest of top (sorted desc) and g (sorted desc); with
-// TRACK, rej <- max(rej, largest key dropped).
+// top <- the 8 largest of top and g (both sorted descending); with TRACK,
+// rej <- max(rej, largest key dropped), i.e. the running 9th largest.
 template <bool TRACK>
 __device__ __forceinline__ void merge8(int (&top)[8], const int (&g)[8], int& rej) {
   int m[8];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    m[i] = max(top[i], g[7 - i]);
-    if (TRACK) rej = max(rej, min(top[i], g[7 - i]));
+  for (int i = 0; i < 8; ++i) m[i] = max(top[i], g[7 - i]);
+  if (TRACK) {
+    const int r0 = max(min(top[0], g[7]), min(top[1], g[6]));
+    const int r1 = max(min(top[2], g[5]), min(top[3], g[4]));
+    const int r2 = max(min(top[4], g[3]), min(top[5], g[2]));
+    const int r3 = max(min(top[6], g[1]), min(top[7], g[0]));
+    rej = max(max(rej, max(r0, r1)), max(r2, r3));
   }
   DOL_CAS(m[0], m[4]) DOL_CAS(m[1], m[5]) DOL_CAS(m[2], m[6]) DOL_CAS(m[3], m[7])
   DOL_CAS(m[0], m[2]) DOL_CAS(m[1], m[3]) DOL_CAS(m[4], m[6]) DOL_CAS(m[5], m[7])
   DOL_CAS(m[0], m[1]) DOL_CAS(m[2], m[3]) DOL_CAS(m[4], m[5]) DOL_CAS(m[6], m[7])
 #pragma unroll
   for (int i = 0; i < 8; ++i) top[i] = m[i];
+}
+
+// Composite keys.  e: expert index (< 256).
+template <bool GEN>
+__device__ __forceinline__ int key_f32(uint32_t u, int e) {
+  if (GEN) u ^= (uint32_t)((int32_t)u >> 31) & 0x7FFFFF00u;
+  return (int)((u & 0xFFFFFF00u) | (uint32_t)(255 - e));
+}
+
+// Two bf16 scores packed in x (element e0 in the low half, e0 + 1 in the high half).
+template <bool GEN>
+__device__ __forceinline__ void key_bf16x2(uint32_t x, int e0, int& lo, int& hi) {
+  if (GEN) {
+    const v2s s = __builtin_bit_cast(v2s, x) >> (short)15;
+    x ^= __builtin_bit_cast(uint32_t, s) & 0x7FFF7FFFu;
+  }
+  lo = (int)((x << 16) | (uint32_t)(255 - e0));
+  hi = (int)((x & 0xFFFF0000u) | (uint32_t)(254 - e0));
+}
+
+// Rank one staged 128-byte chunk (vectors cv0..cv0+7 of the lane's row) into top/rej.
+template <typename T, bool GEN>
+__device__ __forceinline__ void rank_chunk(const unsigned char* sbuf, int lane, int cv0, int (&top)[8], int& rej) {
+  const unsigned char* row = sbuf + lane * 128;
+  const int sw = row_swizzle(lane);
+  auto piece = [&](int q) { return *reinterpret_cast<const v4u*>(row + ((q ^ sw) << 4)); };
+  if (Traits<T>::kVec == 4) {
+#pragma unroll
+    for (int gq = 0; gq < 4; ++gq) {
+      int g[8];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const v4u x = piece(2 * gq + h);
+        const int e0 = (cv0 + 2 * gq + h) * 4;
+        g[4 * h + 0] = key_f32<GEN>(x.x, e0 + 0);
+        g[4 * h + 1] = key_f32<GEN>(x.y, e0 + 1);
+        g[4 * h + 2] = key_f32<GEN>(x.z, e0 + 2);
+        g[4 * h + 3] = key_f32<GEN>(x.w, e0 + 3);
+      }
+      sort8_desc(g);
+      merge8<!Traits<T>::kExact>(top, g, rej);
+    }
+  } else {
+#pragma unroll
+    for (int v = 0; v < 8; ++v) {
+      int g[8];
+      const v4u x = piece(v);
+      const int e0 = (cv0 + v) * 8;
+      key_bf16x2<GEN>(x.x, e0 + 0, g[0], g[1]);
+      key_bf16x2<GEN>(x.y, e0 + 2, g[2], g[3]);
+      key_bf16x2<GEN>(x.z, e0 + 4, g[4], g[5]);
+      key_bf16x2<GEN>(x.w, e0 + 6, g[6], g[7]);
+      sort8_desc(g);
+      merge8<false>(top, g, rej);
+    }
+  }
 }
 
 template <typename T>
@@ -108,20 +193,41 @@ __device__ __forceinline__ uint32_t exact_key(uint32_t u) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// Exact Top-k of one row by k selection passes over unique 64-bit keys
-// (value key, then the complemented index); sets the lane's bit of each
-// chosen expert's word in `bt`.
+__device__ __forceinline__ u64 exact_key64(uint32_t bits, int e) {
+  return ((u64)exact_key(bits) << 32) | (u64)(0xFFFFFFFFu - (uint32_t)e);
+}
+
+// Exact Top-k (k <= 8) of one row in a single pass: insertion of unique
+// 64-bit keys (value key, then the complemented index) into a sorted list.
 template <typename T>
-__device__ void slow_topk_lane(const T* row, int E, int k, u64* bt, u64 bit) {
+__device__ void exact_topk8_lane(const T* row, int E, int k, u64* bt, u64 bit) {
+  u64 lst[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) lst[i] = 0ull;  // every real key is > 0
+  for (int e = 0; e < E; ++e) {
+    const u64 key = exact_key64(elem_bits<T>(row, e), e);
+    if (key <= lst[7]) continue;
+#pragma unroll
+    for (int i = 7; i > 0; --i) lst[i] = max(lst[i], min(lst[i - 1], key));
+    lst[0] = max(lst[0], key);
+  }
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+    if (i < k) atomicOr(&bt[0xFFFFFFFFu - (uint32_t)(lst[i] & 0xFFFFFFFFull)], bit);
+}
+
+// Exact Top-k for any k: k selection passes, each taking the largest key
+// below the previous one.
+template <typename T>
+__device__ void exact_topk_passes_lane(const T* row, int E, int k, u64* bt, u64 bit) {
   u64 prev = ~0ull;
   for (int r = 0; r < k; ++r) {
     u64 best = 0;
     for (int e = 0; e < E; ++e) {
-      const u64 key = ((u64)exact_key(elem_bits<T>(row, e)) << 32) | (u64)(0xFFFFFFFFu - (uint32_t)e);
+      const u64 key = exact_key64(elem_bits<T>(row, e), e);
       if (key < prev && key > best) best = key;
     }
-    const int idx = (int)(0xFFFFFFFFu - (uint32_t)(best & 0xFFFFFFFFull));
-    atomicOr(&bt[idx], bit);
+    atomicOr(&bt[0xFFFFFFFFu - (uint32_t)(best & 0xFFFFFFFFull)], bit);
     prev = best;
   }
 }
@@ -143,14 +249,14 @@ struct PopcGram {
     for (int q = 0; q < MTQ; ++q) {
       int mt = tid + q * NTHREADS;
       int a = -1, b = -1;
-      if (mt < NMT) {
+      if (ON && mt < NMT) {
         a = 0;
         while (mt >= NB - a) {
           mt -= NB - a;
           ++a;
         }
         b = a + mt;
-        if (4 * b >= E) a = b = -1;  // b >= a, so this also drops a >= E/4 blocks
+        if (4 * b >= E) a = b = -1;  // b >= a, so this also drops blocks with a >= E/4
       }
       ra[q] = a;
       rb[q] = b;
@@ -159,10 +265,10 @@ struct PopcGram {
     }
   }
 
-  // bt: nslot signature words per expert, slot-major [nslot][EP]
-  __device__ __forceinline__ void accumulate(const u64* bt, int nslot) {
+  // bt: nslot signature words per expert, slot-major with `stride` words per slot
+  __device__ __forceinline__ void accumulate(const u64* bt, int nslot, int stride) {
     for (int s = 0; s < nslot; ++s) {
-      const u64* w = bt + s * EP;
+      const u64* w = bt + s * stride;
 #pragma unroll
       for (int q = 0; q < MTQ; ++q) {
         if (ra[q] < 0) continue;
@@ -196,46 +302,333 @@ struct PopcGram {
   }
 };
 
+// ---------------------------------------------------------------------------
+// MFMA Gram.  Expert tiles of 32; the tile pairs (I <= J) of the upper
+// triangle are split over the 8 waves so that each wave needs few distinct
+// tiles (each tile costs one bits->bytes expansion per 32 tokens).
+// ---------------------------------------------------------------------------
+constexpr int kMaxPairs = 5;  // per wave
+constexpr int kMaxTiles = 4;  // distinct tiles per wave
+
+struct WavePairs {
+  int nt, np;
+  int tile[kMaxTiles];
+  int pa[kMaxPairs], pb[kMaxPairs];  // indices into tile[]
+};
+
+// T = 8 tiles (E <= 256): 36 pairs, 4-5 pairs and 3-4 tiles per wave.
+constexpr WavePairs kPairs8[8] = {
+    {3, 4, {2, 6, 7, 0}, {0, 0, 1, 2}, {1, 2, 2, 2}},        // (2,6)(2,7)(6,7)(7,7)
+    {4, 5, {1, 3, 5, 7}, {0, 0, 1, 1, 2}, {1, 3, 2, 3, 3}},  // (1,3)(1,7)(3,5)(3,7)(5,7)
+    {3, 4, {4, 5, 6, 0}, {0, 0, 1, 1}, {1, 2, 1, 2}},        // (4,5)(4,6)(5,5)(5,6)
+    {4, 4, {0, 2, 3, 4}, {0, 1, 2, 2}, {2, 2, 2, 3}},        // (0,3)(2,3)(3,3)(3,4)
+    {3, 5, {1, 2, 4, 0}, {0, 0, 1, 1, 2}, {1, 2, 1, 2, 2}},  // (1,2)(1,4)(2,2)(2,4)(4,4)
+    {4, 4, {1, 3, 5, 6}, {0, 0, 1, 3}, {2, 3, 3, 3}},        // (1,5)(1,6)(3,6)(6,6)
+    {4, 5, {0, 1, 2, 5}, {0, 0, 0, 1, 2}, {1, 2, 3, 1, 3}},  // (0,1)(0,2)(0,5)(1,1)(2,5)
+    {4, 5, {0, 4, 6, 7}, {0, 0, 0, 0, 1}, {0, 1, 2, 3, 3}},  // (0,0)(0,4)(0,6)(0,7)(4,7)
+};
+// T = 4 tiles (E <= 128): 10 pairs.
+constexpr WavePairs kPairs4[8] = {
+    {2, 2, {2, 3, 0, 0}, {0, 1}, {1, 1}},  // (2,3)(3,3)
+    {2, 2, {1, 3, 0, 0}, {0, 0}, {0, 1}},  // (1,1)(1,3)
+    {2, 2, {0, 1, 0, 0}, {0, 0}, {0, 1}},  // (0,0)(0,1)
+    {2, 2, {0, 2, 0, 0}, {0, 1}, {1, 1}},  // (0,2)(2,2)
+    {2, 1, {0, 3, 0, 0}, {0}, {1}},        // (0,3)
+    {2, 1, {1, 2, 0, 0}, {0}, {1}},        // (1,2)
+    {0, 0, {0, 0, 0, 0}, {0}, {0}},
+    {0, 0, {0, 0, 0, 0}, {0}, {0}},
+};
+// T = 2 tiles (E <= 64): 3 pairs.
+constexpr WavePairs kPairs2[8] = {
+    {1, 1, {0, 0, 0, 0}, {0}, {0}},  // (0,0)
+    {2, 1, {0, 1, 0, 0}, {0}, {1}},  // (0,1)
+    {1, 1, {1, 0, 0, 0}, {0}, {0}},  // (1,1)
+    {0, 0, {0}, {0}, {0}},
+    {0, 0, {0}, {0}, {0}},
+    {0, 0, {0}, {0}, {0}},
+    {0, 0, {0}, {0}, {0}},
+    {0, 0, {0}, {0}, {0}},
+};
+// T = 1 tile (E <= 32).
+constexpr WavePairs kPairs1[8] = {
+    {1, 1, {0, 0, 0, 0}, {0}, {0}},
+    {0, 0, {0}, {0}, {0}},
+    {0, 0, {0}, {0}, {0}},
+    {0, 0, {0}, {0}, {0}},
+    {0, 0, {0}, {0}, {0}},
+    {0, 0, {0}, {0}, {0}},
+    {0, 0, {0}, {0}, {0}},
+    {0, 0, {0}, {0}, {0}},
+};
+
+template <int T, int W>
+struct PairsOf {
+  static constexpr WavePairs v = T == 8 ? kPairs8[W] : T == 4 ? kPairs4[W] : T == 2 ? kPairs2[W] : kPairs1[W];
+};
+
+// 16 signature bits -> 16 bytes of 0/1 (byte b = bit b).
+__device__ __forceinline__ v4i expand16(uint32_t b) {
+  v4i r;
+  r.x = (int)((((b >> 0) & 0xFu) * 0x00204081u) & 0x01010101u);
+  r.y = (int)((((b >> 4) & 0xFu) * 0x00204081u) & 0x01010101u);
+  r.z = (int)((((b >> 8) & 0xFu) * 0x00204081u) & 0x01010101u);
+  r.w = (int)((((b >> 12) & 0xFu) * 0x00204081u) & 0x01010101u);
+  return r;
+}
+
+// Accumulate the wave's tile pairs over `nslot` words of the bit tile.
+// Lane l covers expert (32*tile + l%32) and, in k-step ks, tokens
+// 32*ks + 16*(l/32) .. +15 of the word; the same expansion feeds both MFMA
+// operands, so A and B always agree on which token each k index is.
+template <int T, int W>
+__device__ __forceinline__ void mfma_wave(v16i (&acc)[kMaxPairs], const u64* bt, int stride, int nslot, int lane) {
+  constexpr WavePairs P = PairsOf<T, W>::v;
+  if (P.np == 0) return;
+  const int el = lane & 31;
+  const int half = lane >> 5;
+  for (int s = 0; s < nslot; ++s) {
+    const uint16_t* w16 = reinterpret_cast<const uint16_t*>(bt + s * stride);
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      v4i f[kMaxTiles];
+#pragma unroll
+      for (int t = 0; t < P.nt; ++t) f[t] = expand16(w16[(P.tile[t] * 32 + el) * 4 + ks * 2 + half]);
+#pragma unroll
+      for (int p = 0; p < P.np; ++p)
+        acc[p] = __builtin_amdgcn_mfma_i32_32x32x32_i8(f[P.pa[p]], f[P.pb[p]], acc[p], 0, 0, 0);
+    }
+  }
+}
+
+template <int T, int W>
+__device__ __forceinline__ void mfma_flush(const v16i (&acc)[kMaxPairs], uint32_t* c, int E, int lane) {
+  constexpr WavePairs P = PairsOf<T, W>::v;
+#pragma unroll
+  for (int p = 0; p < P.np; ++p) {
+    const int I = P.tile[P.pa[p]], J = P.tile[P.pb[p]];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int gi = 32 * I + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      const int gj = 32 * J + (lane & 31);
+      const uint32_t v = (uint32_t)acc[p][r];
+      if (gi <= gj && gj < E && v) atomicAdd(&c[(int64_t)gi * E + gj], v);
+    }
+  }
+}
+
+// One Gram step of wave W: accumulate `nslot` words, then, if `flush`, add the
+// partial counts into c (upper triangle, integer atomics) and restart from 0.
+template <int T, int W>
+__device__ __forceinline__ void mfma_step(v16i (&acc)[kMaxPairs], const u64* bt, int stride, int nslot, int lane,
+                                          bool flush, uint32_t* c, int E) {
+  constexpr WavePairs P = PairsOf<T, W>::v;
+  if (P.np == 0) return;
+  mfma_wave<T, W>(acc, bt, stride, nslot, lane);
+  if (flush) {
+    mfma_flush<T, W>(acc, c, E, lane);
+#pragma unroll
+    for (int p = 0; p < P.np; ++p)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[p][r] = 0;
+  }
+}
+
+template <int T>
+__device__ __forceinline__ void mfma_step_dispatch(int wave, v16i (&acc)[kMaxPairs], const u64* bt, int stride,
+                                                   int nslot, int lane, bool flush, uint32_t* c, int E) {
+  switch (wave) {
+    case 0: mfma_step<T, 0>(acc, bt, stride, nslot, lane, flush, c, E); break;
+    case 1: mfma_step<T, 1>(acc, bt, stride, nslot, lane, flush, c, E); break;
+    case 2: mfma_step<T, 2>(acc, bt, stride, nslot, lane, flush, c, E); break;
+    case 3: mfma_step<T, 3>(acc, bt, stride, nslot, lane, flush, c, E); break;
+    case 4: mfma_step<T, 4>(acc, bt, stride, nslot, lane, flush, c, E); break;
+    case 5: mfma_step<T, 5>(acc, bt, stride, nslot, lane, flush, c, E); break;
+    case 6: mfma_step<T, 6>(acc, bt, stride, nslot, lane, flush, c, E); break;
+    default: mfma_step<T, 7>(acc, bt, stride, nslot, lane, flush, c, E); break;
+  }
+}
+
+template <int T>
+__device__ __forceinline__ void mfma_dispatch(int wave, v16i (&acc)[kMaxPairs], const u64* bt, int stride, int nslot,
+                                              int lane) {
+  switch (wave) {
+    case 0: mfma_wave<T, 0>(acc, bt, stride, nslot, lane); break;
+    case 1: mfma_wave<T, 1>(acc, bt, stride, nslot, lane); break;
+    case 2: mfma_wave<T, 2>(acc, bt, stride, nslot, lane); break;
+    case 3: mfma_wave<T, 3>(acc, bt, stride, nslot, lane); break;
+    case 4: mfma_wave<T, 4>(acc, bt, stride, nslot, lane); break;
+    case 5: mfma_wave<T, 5>(acc, bt, stride, nslot, lane); break;
+    case 6: mfma_wave<T, 6>(acc, bt, stride, nslot, lane); break;
+    default: mfma_wave<T, 7>(acc, bt, stride, nslot, lane); break;
+  }
+}
+
+template <int T>
+__device__ __forceinline__ void mfma_flush_dispatch(int wave, const v16i (&acc)[kMaxPairs], uint32_t* c, int E,
+                                                    int lane) {
+  switch (wave) {
+    case 0: mfma_flush<T, 0>(acc, c, E, lane); break;
+    case 1: mfma_flush<T, 1>(acc, c, E, lane); break;
+    case 2: mfma_flush<T, 2>(acc, c, E, lane); break;
+    case 3: mfma_flush<T, 3>(acc, c, E, lane); break;
+    case 4: mfma_flush<T, 4>(acc, c, E, lane); break;
+    case 5: mfma_flush<T, 5>(acc, c, E, lane); break;
+    case 6: mfma_flush<T, 6>(acc, c, E, lane); break;
+    default: mfma_flush<T, 7>(acc, c, E, lane); break;
+  }
+}
+
 #define DOL_WAVE_FENCE() asm volatile("" ::: "memory")
 
+// Per-segment view used by the kernel.
+struct SegView {
+  const unsigned char* base;
+  int64_t n, off, w_first, t_begin, t_end;  // t_begin/t_end: the segment's range of global words
+  int layer;
+};
+
+__device__ __forceinline__ SegView seg_view(const SegTable& tab, int i) {
+  SegView v;
+  v.base = reinterpret_cast<const unsigned char*>(tab.s[i].scores);
+  v.n = tab.s[i].n;
+  v.off = tab.s[i].tok_off;
+  v.w_first = v.off >> 6;
+  v.t_begin = tab.tile_start[i];
+  v.t_end = tab.tile_start[i + 1];
+  v.layer = tab.s[i].layer;
+  return v;
+}
+
+// Segment holding global word g (segments with no words are skipped).
+__device__ __forceinline__ int seg_of(const SegTable& tab, int64_t g, int from) {
+  int i = from;
+  while (i + 1 < tab.nseg && g >= tab.tile_start[i + 1]) ++i;
+  return i;
+}
+
 // ---------------------------------------------------------------------------
-// Top-K (+ Gram) kernel.  grid = (blocks per segment, segments).
+// Top-K (+ Gram) kernel.  One persistent block per CU slot; block b owns the
+// contiguous range [b*T/G, (b+1)*T/G) of the T global signature words of the
+// launch and walks it 8 words (one per wave) at a time, never mixing two
+// segments in one step.  Gram accumulators are flushed whenever the next step
+// belongs to another layer, and at the end.
+// flags bit 0: fast path allowed (16-byte rows, k <= 8, E <= 256).
 // ---------------------------------------------------------------------------
-template <typename T, int EP, bool GRAM>
-__global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab, const PathArgs a, int fast) {
-  constexpr int VEC = Traits<T>::kVec;
+template <typename T, int EP, int GM>
+__global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab, const PathArgs a, int flags) {
+  constexpr int EPW = EP < 32 ? 32 : EP;  // signature words per slot of the bit tile
+  constexpr int NT = EPW / 32;            // 32-expert tiles
   extern __shared__ __align__(16) unsigned char smem[];
-  unsigned char* stage_all = smem;                                                  // [waves][64][stride]
-  u64* bt_all = reinterpret_cast<u64*>(smem + (fast ? kFusedWaves * 64 * kStageStride : 0));  // [waves][EP]
+  const bool fast = (flags & 1) != 0;
+  unsigned char* stage_all = smem;
+  u64* bt_all = reinterpret_cast<u64*>(smem + (fast ? kStageBytes : 0));  // [2][kFusedWaves][EPW]
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const Segment sg = tab.s[blockIdx.y];
   const int E = a.E, k = a.k;
-  const int64_t n = sg.n, off = sg.tok_off;
-  if (n <= 0) return;
-  const int64_t w_first = off >> 6;
-  const int64_t ntile = ((off + n - 1) >> 6) - w_first + 1;
   const int rowB = E * (int)sizeof(T);
   const int rowv = rowB >> 4;
   const int nch = (rowv + 7) >> 3;
-  const unsigned char* base = reinterpret_cast<const unsigned char*>(sg.scores);
-  unsigned char* st = stage_all + wave * 64 * kStageStride;
-  u64* mybt = bt_all + wave * EP;
+  unsigned char* st = stage_all + wave * 2 * kChunkBytes;  // this wave's two stage buffers
 
-  PopcGram<EP, kFusedThreads, GRAM> gram;
-  if (GRAM) gram.init(tid, E);
+  const int64_t T_all = tab.tile_start[tab.nseg];
+  const int64_t gs = (int64_t)blockIdx.x * T_all / gridDim.x;
+  const int64_t ge = (int64_t)(blockIdx.x + 1) * T_all / gridDim.x;
+  if (gs >= ge) return;
 
-  for (int64_t tb = (int64_t)blockIdx.x * kFusedWaves; tb < ntile; tb += (int64_t)gridDim.x * kFusedWaves) {
-    const int64_t tile = tb + wave;
+  PopcGram<EPW, kFusedThreads, GM == kGramPopc> pg;
+  if (GM == kGramPopc) pg.init(tid, E);
+  v16i acc[kMaxPairs];
+  auto zero_acc = [&]() {
 #pragma unroll
-    for (int e0 = 0; e0 < EP; e0 += 64)
-      if (e0 + lane < EP) mybt[e0 + lane] = 0;
+    for (int p = 0; p < kMaxPairs; ++p)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[p][r] = 0;
+  };
+  zero_acc();
+
+  // Lane offsets inside a chunk: instruction j fills rows 8j..8j+7; lane i
+  // fills slot (i & 7) of row 8j + i/8, which holds piece
+  // q = (i & 7) ^ swz(8j + i/8) = (i & 7) ^ (i >> 3) ^ (j & 1).
+  const int q_even = (lane & 7) ^ (lane >> 3);
+  const uint32_t off_even = (uint32_t)((lane >> 3) * rowB + q_even * 16);        // bytes from the chunk's row 0
+  const uint32_t off_odd = (uint32_t)((lane >> 3) * rowB + (q_even ^ 1) * 16);  // odd j: piece q_even ^ 1
+
+  // Direct-to-LDS load of a full 64-row x 128-byte chunk of local word `tl` of
+  // segment `sv` (asynchronous; the consumer waits with DOL_WAIT_VMEM).
+  auto dma = [&](const SegView& sv, int64_t tl, int c_, unsigned char* sbuf) {
+    if (c_ * 8 + 8 > rowv) return;
+    const int64_t t0_ = (sv.w_first + tl) * 64 - sv.off;
+    const unsigned char* cbase = sv.base + t0_ * rowB + c_ * 128;  // row 0 of the chunk (uniform)
+    if (t0_ >= 0 && t0_ + 64 <= sv.n) {  // every row inside the segment
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        __builtin_amdgcn_global_load_lds(cbase + (uint32_t)(j * 8 * rowB) + ((j & 1) ? off_odd : off_even),
+                                         (__attribute__((address_space(3))) void*)(sbuf + j * 1024), 16, 0, 0);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int64_t tr = t0_ + 8 * j + (lane >> 3);
+        if (tr >= 0 && tr < sv.n)
+          __builtin_amdgcn_global_load_lds(cbase + (uint32_t)(j * 8 * rowB) + ((j & 1) ? off_odd : off_even),
+                                           (__attribute__((address_space(3))) void*)(sbuf + j * 1024), 16, 0, 0);
+      }
+    }
+  };
+  // Synchronous fill of a partial chunk (the row ends inside it): missing
+  // vectors read as all-ones (a NaN), ranked last and never selected on the fast path.
+  auto fill_partial = [&](const SegView& sv, int64_t t0_, int c_, unsigned char* sbuf) {
+    const int cvn = rowv - c_ * 8;
+    const unsigned char* cbase = sv.base + t0_ * rowB + c_ * 128;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int64_t tr = t0_ + 8 * j + (lane >> 3);
+      const int q = q_even ^ (j & 1);
+      v4u val = v4u{~0u, ~0u, ~0u, ~0u};
+      if (q < cvn && tr >= 0 && tr < sv.n)
+        val = *reinterpret_cast<const v4u*>(cbase + (uint32_t)(j * 8 * rowB) + ((j & 1) ? off_odd : off_even));
+      *reinterpret_cast<v4u*>(sbuf + j * 1024 + lane * 16) = val;
+    }
+  };
+
+  // General keys cost bf16 ~0.75 extra instructions per score and fp32 ~3, so
+  // bf16 starts with them; an fp32 wave switches after meeting a non-positive threshold.
+  bool gen = Traits<T>::kExact;
+  int cb = 0;  // stage buffer holding the current chunk
+
+  int seg = seg_of(tab, gs, 0);
+  SegView sv = seg_view(tab, seg);
+  if (fast && gs + wave < min(ge, sv.t_end)) dma(sv, gs + wave - sv.t_begin, 0, st);
+
+  int buf = 0;
+  int64_t p = gs;
+  while (p < ge) {  // one run of steps within one layer, then a flush
+  const int run_layer = sv.layer;
+  for (; p < ge && sv.layer == run_layer; buf ^= 1) {
+    const int64_t cnt = min((int64_t)kFusedWaves, min(ge, sv.t_end) - p);  // words in this step
+    // position and segment of the next step (block-uniform)
+    const int64_t pn = p + cnt;
+    const int seg_n = (pn < ge) ? seg_of(tab, pn, seg) : seg;
+    const SegView svn = seg_view(tab, seg_n);
+    const bool next_mine = pn + wave < min(ge, svn.t_end);
+
+    u64* bt = bt_all + buf * kFusedWaves * EPW;
+    u64* mybt = bt + wave * EPW;
+#pragma unroll
+    for (int e0 = 0; e0 < EPW; e0 += 64)
+      if (e0 + lane < EPW) mybt[e0 + lane] = 0;
     DOL_WAVE_FENCE();
-    if (tile < ntile) {
-      const int64_t w = w_first + tile;
-      const int64_t t0 = w * 64 - off;  // token of lane 0 (negative in a history's first partial word)
+    const int64_t tl0 = p - sv.t_begin;  // local word of slot 0
+    if (fast && wave >= cnt && next_mine) {
+      // idle this step (segment end) but busy in the next one, which may lie in
+      // another segment: start that tile's first chunk now, into the buffer the
+      // next step reads first
+      dma(svn, pn + wave - svn.t_begin, 0, st + cb * kChunkBytes);
+    }
+    if (wave < cnt) {
+      const int64_t tl = tl0 + wave;
+      const int64_t t0 = (sv.w_first + tl) * 64 - sv.off;  // token of lane 0 (negative in a history's first partial word)
       const int64_t t = t0 + lane;
-      const bool valid = (t >= 0) && (t < n);
+      const bool valid = (t >= 0) && (t < sv.n);
       bool need_slow = valid;
       if (fast) {
         int top[8];
@@ -243,67 +636,39 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab, cons
 #pragma unroll
         for (int i = 0; i < 8; ++i) top[i] = INT_MIN;
         for (int c = 0; c < nch; ++c) {
-          const int cv0 = c * 8;
-          const int cvn = min(8, rowv - cv0);
-          // cooperative, coalesced load of a 64-row x 128-byte chunk into LDS
-#pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const int flat = j * 64 + lane;
-            const int r = flat >> 3, v = flat & 7;
-            const int64_t tr = t0 + r;
-            if (v < cvn && tr >= 0 && tr < n) {
-              const v4u val = __builtin_nontemporal_load(
-                  reinterpret_cast<const v4u*>(base + tr * rowB + (int64_t)(cv0 + v) * 16));
-              *reinterpret_cast<v4u*>(st + r * kStageStride + v * 16) = val;
-            }
-          }
-          DOL_WAVE_FENCE();
-          v4u vv[8];
-#pragma unroll
-          for (int v = 0; v < 8; ++v) vv[v] = *reinterpret_cast<const v4u*>(st + lane * kStageStride + v * 16);
-          DOL_WAVE_FENCE();
-          if (VEC == 4) {
-#pragma unroll
-            for (int gq = 0; gq < 4; ++gq) {
-              int g[8];
-#pragma unroll
-              for (int h = 0; h < 2; ++h) {
-                const int v = 2 * gq + h;
-                const v4u x = vv[v];
-                const uint32_t xs[4] = {x.x, x.y, x.z, x.w};
-                const int e0 = (cv0 + v) * 4;
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                  g[h * 4 + i] = (v < cvn) ? composite(xs[i], Traits<T>::kHiMask, e0 + i) : INT_MIN;
-              }
-              sort8_desc(g);
-              merge8<!Traits<T>::kExact>(top, g, rej);
-            }
+          unsigned char* cur = st + cb * kChunkBytes;
+          if (c * 8 + 8 <= rowv) {
+            DOL_WAIT_VMEM();  // this chunk's direct-to-LDS loads have landed
           } else {
-#pragma unroll
-            for (int v = 0; v < 8; ++v) {
-              int g[8];
-              const v4u x = vv[v];
-              const uint32_t xs[4] = {x.x, x.y, x.z, x.w};
-              const int e0 = (cv0 + v) * 8;
-#pragma unroll
-              for (int i = 0; i < 4; ++i) {
-                g[2 * i] = (v < cvn) ? composite(xs[i] << 16, Traits<T>::kHiMask, e0 + 2 * i) : INT_MIN;
-                g[2 * i + 1] = (v < cvn) ? composite(xs[i] & 0xFFFF0000u, Traits<T>::kHiMask, e0 + 2 * i + 1) : INT_MIN;
-              }
-              sort8_desc(g);
-              merge8<!Traits<T>::kExact>(top, g, rej);
-            }
+            fill_partial(sv, t0, c, cur);
           }
+          DOL_WAVE_FENCE();
+          unsigned char* other = st + (cb ^ 1) * kChunkBytes;
+          if (c + 1 < nch)
+            dma(sv, tl, c + 1, other);
+          else if (next_mine)
+            dma(svn, pn + wave - svn.t_begin, 0, other);
+          if (gen)
+            rank_chunk<T, true>(cur, lane, c * 8, top, rej);
+          else
+            rank_chunk<T, false>(cur, lane, c * 8, top, rej);
+          DOL_WAVE_FENCE();
+          cb ^= 1;
         }
-        // threshold checks (k <= 8 on this path)
         int sk = INT_MIN, sk1 = rej;
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
           sk = (i == k - 1) ? top[i] : sk;
           sk1 = (i == k) ? top[i] : sk1;
         }
-        bool ok = (top[0] < kCompPosInf) && (sk > kCompNegInfMax) && (sk < Traits<T>::kZeroLo || sk > Traits<T>::kZeroHi);
+        bool ok = top[0] < kCompPosInf;
+        bool nonpos = false;
+        if (gen) {
+          ok = ok && sk > kCompNegInfMax && (sk < Traits<T>::kZeroLo || sk > Traits<T>::kZeroHi);
+        } else {
+          nonpos = valid && sk < Traits<T>::kPosMin;
+          ok = ok && !nonpos;
+        }
         if (!Traits<T>::kExact) ok = ok && ((sk1 >> 8) < (sk >> 8));
         need_slow = valid && !ok;
         if (valid && ok) {
@@ -312,88 +677,116 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab, cons
           for (int i = 0; i < 8; ++i)
             if (i < k) atomicOr(&mybt[255 - (top[i] & 255)], bit);
         }
+        if (__ballot(nonpos) != 0ull) gen = true;
       }
       if (__ballot(need_slow) != 0ull) {
-        if (need_slow)
-          slow_topk_lane<T>(reinterpret_cast<const T*>(base) + t * (int64_t)E, E, k, mybt, 1ull << lane);
-      }
-      DOL_WAVE_FENCE();
-      if (a.bits != nullptr) {
-        u64* dst = a.bits + (int64_t)sg.layer * a.bits_layer_words + w;
-        const bool full = (t0 >= 0) && (t0 + 64 <= n);
-        for (int e = lane; e < E; e += 64) {
-          const u64 word = mybt[e];
-          if (full || !a.or_partial)
-            dst[(int64_t)e * a.W] = word;
-          else if (word)
-            atomicOr(dst + (int64_t)e * a.W, word);
+        if (need_slow) {
+          const T* row = reinterpret_cast<const T*>(sv.base) + t * (int64_t)E;
+          if (k <= 8)
+            exact_topk8_lane<T>(row, E, k, mybt, 1ull << lane);
+          else
+            exact_topk_passes_lane<T>(row, E, k, mybt, 1ull << lane);
         }
       }
     }
-    if (GRAM) {
-      __syncthreads();
-      gram.accumulate(bt_all, kFusedWaves);
-      __syncthreads();
+    __syncthreads();
+    // signatures: up to 8 consecutive words per expert, written as 64-byte runs
+    if (a.bits != nullptr) {
+      u64* lb = a.bits + (int64_t)sv.layer * a.bits_layer_words;
+      for (int item = tid; item < E * kFusedWaves; item += kFusedThreads) {
+        const int e = item >> 3, s = item & 7;
+        if (s >= cnt) continue;
+        const int64_t w = sv.w_first + tl0 + s;
+        const int64_t t0s = w * 64 - sv.off;
+        const u64 word = bt[s * EPW + e];
+        u64* dst = lb + (int64_t)e * a.W + w;
+        if (!a.or_partial || (t0s >= 0 && t0s + 64 <= sv.n))
+          *dst = word;
+        else if (word)
+          atomicOr(dst, word);
+      }
+    }
+    if (GM == kGramMfma) mfma_dispatch<NT>(wave, acc, bt, EPW, kFusedWaves, lane);  // empty slots are zero
+    if (GM == kGramPopc) pg.accumulate(bt, (int)cnt, EPW);
+    p = pn;
+    seg = seg_n;
+    sv = svn;
+  }
+  if (GM != kGramNone) {
+    uint32_t* cl = a.cacc + (int64_t)run_layer * a.cacc_layer_elems;
+    if (GM == kGramMfma) {
+      mfma_flush_dispatch<NT>(wave, acc, cl, E, lane);
+      zero_acc();
+    }
+    if (GM == kGramPopc) {
+      pg.flush(cl, E);
+      pg.init(tid, E);
     }
   }
-  if (GRAM) gram.flush(a.cacc + (int64_t)sg.layer * a.cacc_layer_elems, E);
+  }
 }
 
-template <typename T, int EP, bool GRAM>
-hipError_t launch_one(const SegTable& tab, int nseg, int64_t max_seg_tokens, const PathArgs& a, bool fast,
-                      hipStream_t s) {
-  auto kern = k_topk<T, EP, GRAM>;
-  const size_t lds = (fast ? (size_t)kFusedWaves * 64 * kStageStride : 0) + (size_t)kFusedWaves * EP * sizeof(u64);
+int g_gram_mode = -1;  // kGramPopc or kGramMfma; read once from DOLOSS_GRAM ("popc" selects popcount)
+
+int gram_mode() {
+  if (g_gram_mode < 0) {
+    const char* v = getenv("DOLOSS_GRAM");
+    g_gram_mode = (v != nullptr && v[0] == 'p') ? kGramPopc : kGramMfma;
+  }
+  return g_gram_mode;
+}
+
+template <typename T, int EP, int GM>
+hipError_t launch_one(const SegTable& tab, const PathArgs& a, bool fast, hipStream_t s) {
+  constexpr int EPW = EP < 32 ? 32 : EP;
+  auto kern = k_topk<T, EP, GM>;
+  const size_t lds = (fast ? (size_t)kStageBytes : 0) + 2 * (size_t)kFusedWaves * EPW * sizeof(u64);
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   int occ = 1;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kern, kFusedThreads, lds) != hipSuccess || occ < 1) occ = 1;
   const DevInfo di = device_info();
-  const int64_t tiles = (max_seg_tokens + 63) / 64 + 1;
-  int64_t bx = ((int64_t)di.cu_count * occ + nseg - 1) / nseg;
-  bx = std::min<int64_t>(bx, (tiles + kFusedWaves - 1) / kFusedWaves);
-  bx = std::max<int64_t>(bx, 1);
-  hipLaunchKernelGGL(kern, dim3((unsigned)bx, (unsigned)nseg), dim3(kFusedThreads), lds, s, tab, a, fast ? 1 : 0);
+  const int64_t words = tab.tile_start[tab.nseg];
+  int64_t blocks = std::min<int64_t>((int64_t)di.cu_count * occ, (words + kFusedWaves - 1) / kFusedWaves);
+  blocks = std::max<int64_t>(blocks, 1);
+  hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kFusedThreads), lds, s, tab, a, fast ? 1 : 0);
   return hipGetLastError();
 }
 
-template <typename T, bool GRAM>
-hipError_t launch_ep(const SegTable& tab, int nseg, int64_t max_seg_tokens, const PathArgs& a, bool fast,
-                     hipStream_t s) {
-  const int E = a.E;
-  if (E <= 8) return launch_one<T, 8, GRAM>(tab, nseg, max_seg_tokens, a, fast, s);
-  if (E <= 16) return launch_one<T, 16, GRAM>(tab, nseg, max_seg_tokens, a, fast, s);
-  if (E <= 32) return launch_one<T, 32, GRAM>(tab, nseg, max_seg_tokens, a, fast, s);
-  if (E <= 64) return launch_one<T, 64, GRAM>(tab, nseg, max_seg_tokens, a, fast, s);
-  if (E <= 128) return launch_one<T, 128, GRAM>(tab, nseg, max_seg_tokens, a, fast, s);
-  if (E <= 256) return launch_one<T, 256, GRAM>(tab, nseg, max_seg_tokens, a, fast, s);
-  return hipErrorInvalidValue;
+template <typename T, int EP>
+hipError_t launch_gm(const SegTable& tab, const PathArgs& a, bool fast, hipStream_t s) {
+  if (a.cacc == nullptr) return launch_one<T, EP, kGramNone>(tab, a, fast, s);
+  if (gram_mode() == kGramPopc) return launch_one<T, EP, kGramPopc>(tab, a, fast, s);
+  return launch_one<T, EP, kGramMfma>(tab, a, fast, s);
 }
 
 template <typename T>
-hipError_t launch_slow_wide(const SegTable& tab, int nseg, int64_t max_seg_tokens, const PathArgs& a, hipStream_t s) {
-  // E in (256, 1024]: exact per-lane selection, signatures only.
-  if (a.E <= 512) return launch_one<T, 512, false>(tab, nseg, max_seg_tokens, a, false, s);
-  return launch_one<T, 1024, false>(tab, nseg, max_seg_tokens, a, false, s);
+hipError_t launch_ep(const SegTable& tab, const PathArgs& a, bool fast, hipStream_t s) {
+  const int E = a.E;
+  if (E <= 32) return launch_gm<T, 32>(tab, a, fast, s);
+  if (E <= 64) return launch_gm<T, 64>(tab, a, fast, s);
+  if (E <= 128) return launch_gm<T, 128>(tab, a, fast, s);
+  if (E <= 256) return launch_gm<T, 256>(tab, a, fast, s);
+  // E in (256, 1024]: exact per-lane selection, signatures only
+  if (a.cacc != nullptr) return hipErrorInvalidValue;
+  if (E <= 512) return launch_one<T, 512, kGramNone>(tab, a, false, s);
+  return launch_one<T, 1024, kGramNone>(tab, a, false, s);
 }
 
 }  // namespace
 
-hipError_t launch_topk(do_dtype dt, const SegTable& tab, int nseg, int64_t max_seg_tokens, const PathArgs& a,
-                       bool fast_ok, hipStream_t s) {
-  const bool gram = a.cacc != nullptr;
-  const bool fast = fast_ok && a.k <= kFastMaxK && a.E <= kFastMaxE;
-  if (a.E > kFastMaxE) {
-    if (gram) return hipErrorInvalidValue;
-    return dt == DO_F32 ? launch_slow_wide<float>(tab, nseg, max_seg_tokens, a, s)
-                        : launch_slow_wide<uint16_t>(tab, nseg, max_seg_tokens, a, s);
+hipError_t launch_topk(do_dtype dt, SegTable& tab, int nseg, const PathArgs& a, bool fast_ok, hipStream_t s) {
+  tab.nseg = nseg;
+  tab.tile_start[0] = 0;
+  for (int i = 0; i < nseg; ++i) {
+    const int64_t n = tab.s[i].n, off = tab.s[i].tok_off;
+    const int64_t words = n > 0 ? ((off + n - 1) >> 6) - (off >> 6) + 1 : 0;
+    tab.tile_start[i + 1] = tab.tile_start[i] + words;
   }
-  if (dt == DO_F32)
-    return gram ? launch_ep<float, true>(tab, nseg, max_seg_tokens, a, fast, s)
-                : launch_ep<float, false>(tab, nseg, max_seg_tokens, a, fast, s);
-  return gram ? launch_ep<uint16_t, true>(tab, nseg, max_seg_tokens, a, fast, s)
-              : launch_ep<uint16_t, false>(tab, nseg, max_seg_tokens, a, fast, s);
+  if (tab.tile_start[nseg] == 0) return hipSuccess;
+  const bool fast = fast_ok && a.k <= kFastMaxK && a.E <= kFastMaxE;
+  return dt == DO_F32 ? launch_ep<float>(tab, a, fast, s) : launch_ep<uint16_t>(tab, a, fast, s);
 }
 
 }  // namespace dol
