@@ -28,9 +28,10 @@ struct Segment {
   int32_t pad_;
 };
 
-// Segments of one launch.  tile_start[i] is the number of 64-position
-// signature words of segments 0..i-1 (filled by launch_topk): the blocks of a
-// launch split the concatenated word range [0, tile_start[nseg]) evenly.
+// Segments of one launch.  tile_start[i] is the number of 8-word units
+// (512 output positions, 8-aligned within their segment) of segments
+// 0..i-1, filled by launch_topk: the blocks of a launch split the
+// concatenated unit range [0, tile_start[nseg]) evenly.
 struct SegTable {
   Segment s[kMaxSeg];
   int64_t tile_start[kMaxSeg + 1];

@@ -55,6 +55,17 @@ constexpr int kStageBytes = kFusedWaves * 2 * kChunkBytes;
 
 __device__ __forceinline__ int row_swizzle(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
+// The signature word of expert e in slot s of the bit tile lives at index
+// e ^ bt_swz(s): the 8 words of one expert then sit in 8 different banks
+// (the signature output reads them together), and 4-aligned groups and
+// 32-expert tiles stay intact for the Gram readers.
+__device__ __forceinline__ int bt_swz(int s) { return (s & 7) << 2; }
+
+// Cache policy of the score loads: non-temporal (the "slc" bit, nt on gfx950), so
+// the read-once stream ages out of L2 before the partially written signature
+// lines, which then merge there into whole lines before eviction.
+constexpr int kStreamPolicy = 2;
+
 // s_waitcnt vmcnt(0) (expcnt and lgkmcnt left at their maxima)
 #define DOL_WAIT_VMEM() __builtin_amdgcn_s_waitcnt(0x0F70)
 
@@ -119,27 +130,37 @@ __device__ __forceinline__ void merge8(int (&top)[8], const int (&g)[8], int& re
   for (int i = 0; i < 8; ++i) top[i] = m[i];
 }
 
-// Composite keys.  e: expert index (< 256).
+// (x & mask) | (y & ~mask) in one instruction.  Written out because the
+// compiler otherwise splits it into AND + OR: gfx9 VOP3 encodings take no
+// literal, so the mask sits in a VGPR and the expert index in an SGPR.
+__device__ __forceinline__ uint32_t bfi(uint32_t vmask, uint32_t x, uint32_t sidx) {
+  uint32_t r;
+  asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(r) : "v"(vmask), "v"(x), "s"(sidx));
+  return r;
+}
+
+// Composite keys.  e: expert index (< 256).  vm24 = 0xFFFFFF00, vm16 = 0xFFFF0000 (VGPRs).
 template <bool GEN>
-__device__ __forceinline__ int key_f32(uint32_t u, int e) {
+__device__ __forceinline__ int key_f32(uint32_t u, int e, uint32_t vm24) {
   if (GEN) u ^= (uint32_t)((int32_t)u >> 31) & 0x7FFFFF00u;
-  return (int)((u & 0xFFFFFF00u) | (uint32_t)(255 - e));
+  return (int)bfi(vm24, u, (uint32_t)(255 - e));
 }
 
 // Two bf16 scores packed in x (element e0 in the low half, e0 + 1 in the high half).
 template <bool GEN>
-__device__ __forceinline__ void key_bf16x2(uint32_t x, int e0, int& lo, int& hi) {
+__device__ __forceinline__ void key_bf16x2(uint32_t x, int e0, uint32_t vm16, int& lo, int& hi) {
   if (GEN) {
     const v2s s = __builtin_bit_cast(v2s, x) >> (short)15;
     x ^= __builtin_bit_cast(uint32_t, s) & 0x7FFF7FFFu;
   }
   lo = (int)((x << 16) | (uint32_t)(255 - e0));
-  hi = (int)((x & 0xFFFF0000u) | (uint32_t)(254 - e0));
+  hi = (int)bfi(vm16, x, (uint32_t)(254 - e0));
 }
 
 // Rank one staged 128-byte chunk (vectors cv0..cv0+7 of the lane's row) into top/rej.
 template <typename T, bool GEN>
-__device__ __forceinline__ void rank_chunk(const unsigned char* sbuf, int lane, int cv0, int (&top)[8], int& rej) {
+__device__ __forceinline__ void rank_chunk(const unsigned char* sbuf, int lane, int cv0, uint32_t vmask,
+                                           int (&top)[8], int& rej) {
   const unsigned char* row = sbuf + lane * 128;
   const int sw = row_swizzle(lane);
   auto piece = [&](int q) { return *reinterpret_cast<const v4u*>(row + ((q ^ sw) << 4)); };
@@ -151,10 +172,10 @@ __device__ __forceinline__ void rank_chunk(const unsigned char* sbuf, int lane, 
       for (int h = 0; h < 2; ++h) {
         const v4u x = piece(2 * gq + h);
         const int e0 = (cv0 + 2 * gq + h) * 4;
-        g[4 * h + 0] = key_f32<GEN>(x.x, e0 + 0);
-        g[4 * h + 1] = key_f32<GEN>(x.y, e0 + 1);
-        g[4 * h + 2] = key_f32<GEN>(x.z, e0 + 2);
-        g[4 * h + 3] = key_f32<GEN>(x.w, e0 + 3);
+        g[4 * h + 0] = key_f32<GEN>(x.x, e0 + 0, vmask);
+        g[4 * h + 1] = key_f32<GEN>(x.y, e0 + 1, vmask);
+        g[4 * h + 2] = key_f32<GEN>(x.z, e0 + 2, vmask);
+        g[4 * h + 3] = key_f32<GEN>(x.w, e0 + 3, vmask);
       }
       sort8_desc(g);
       merge8<!Traits<T>::kExact>(top, g, rej);
@@ -165,10 +186,10 @@ __device__ __forceinline__ void rank_chunk(const unsigned char* sbuf, int lane, 
       int g[8];
       const v4u x = piece(v);
       const int e0 = (cv0 + v) * 8;
-      key_bf16x2<GEN>(x.x, e0 + 0, g[0], g[1]);
-      key_bf16x2<GEN>(x.y, e0 + 2, g[2], g[3]);
-      key_bf16x2<GEN>(x.z, e0 + 4, g[4], g[5]);
-      key_bf16x2<GEN>(x.w, e0 + 6, g[6], g[7]);
+      key_bf16x2<GEN>(x.x, e0 + 0, vmask, g[0], g[1]);
+      key_bf16x2<GEN>(x.y, e0 + 2, vmask, g[2], g[3]);
+      key_bf16x2<GEN>(x.z, e0 + 4, vmask, g[4], g[5]);
+      key_bf16x2<GEN>(x.w, e0 + 6, vmask, g[6], g[7]);
       sort8_desc(g);
       merge8<false>(top, g, rej);
     }
@@ -200,7 +221,7 @@ __device__ __forceinline__ u64 exact_key64(uint32_t bits, int e) {
 // Exact Top-k (k <= 8) of one row in a single pass: insertion of unique
 // 64-bit keys (value key, then the complemented index) into a sorted list.
 template <typename T>
-__device__ void exact_topk8_lane(const T* row, int E, int k, u64* bt, u64 bit) {
+__device__ void exact_topk8_lane(const T* row, int E, int k, u64* bt, int swz, u64 bit) {
   u64 lst[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) lst[i] = 0ull;  // every real key is > 0
@@ -213,13 +234,13 @@ __device__ void exact_topk8_lane(const T* row, int E, int k, u64* bt, u64 bit) {
   }
 #pragma unroll
   for (int i = 0; i < 8; ++i)
-    if (i < k) atomicOr(&bt[0xFFFFFFFFu - (uint32_t)(lst[i] & 0xFFFFFFFFull)], bit);
+    if (i < k) atomicOr(&bt[(int)(0xFFFFFFFFu - (uint32_t)(lst[i] & 0xFFFFFFFFull)) ^ swz], bit);
 }
 
 // Exact Top-k for any k: k selection passes, each taking the largest key
 // below the previous one.
 template <typename T>
-__device__ void exact_topk_passes_lane(const T* row, int E, int k, u64* bt, u64 bit) {
+__device__ void exact_topk_passes_lane(const T* row, int E, int k, u64* bt, int swz, u64 bit) {
   u64 prev = ~0ull;
   for (int r = 0; r < k; ++r) {
     u64 best = 0;
@@ -227,7 +248,7 @@ __device__ void exact_topk_passes_lane(const T* row, int E, int k, u64* bt, u64 
       const u64 key = exact_key64(elem_bits<T>(row, e), e);
       if (key < prev && key > best) best = key;
     }
-    atomicOr(&bt[0xFFFFFFFFu - (uint32_t)(best & 0xFFFFFFFFull)], bit);
+    atomicOr(&bt[(int)(0xFFFFFFFFu - (uint32_t)(best & 0xFFFFFFFFull)) ^ swz], bit);
     prev = best;
   }
 }
@@ -272,10 +293,11 @@ struct PopcGram {
 #pragma unroll
       for (int q = 0; q < MTQ; ++q) {
         if (ra[q] < 0) continue;
-        const ulonglong2 a01 = *reinterpret_cast<const ulonglong2*>(w + 4 * ra[q]);
-        const ulonglong2 a23 = *reinterpret_cast<const ulonglong2*>(w + 4 * ra[q] + 2);
-        const ulonglong2 b01 = *reinterpret_cast<const ulonglong2*>(w + 4 * rb[q]);
-        const ulonglong2 b23 = *reinterpret_cast<const ulonglong2*>(w + 4 * rb[q] + 2);
+        const int ga = (4 * ra[q]) ^ bt_swz(s), gb = (4 * rb[q]) ^ bt_swz(s);
+        const ulonglong2 a01 = *reinterpret_cast<const ulonglong2*>(w + ga);
+        const ulonglong2 a23 = *reinterpret_cast<const ulonglong2*>(w + ga + 2);
+        const ulonglong2 b01 = *reinterpret_cast<const ulonglong2*>(w + gb);
+        const ulonglong2 b23 = *reinterpret_cast<const ulonglong2*>(w + gb + 2);
         const u64 A[4] = {a01.x, a01.y, a23.x, a23.y};
         const u64 B[4] = {b01.x, b01.y, b23.x, b23.y};
 #pragma unroll
@@ -307,7 +329,9 @@ struct PopcGram {
 // triangle are split over the 8 waves so that each wave needs few distinct
 // tiles (each tile costs one bits->bytes expansion per 32 tokens).
 // ---------------------------------------------------------------------------
-constexpr int kMaxPairs = 5;  // per wave
+constexpr int kMaxPairs = 5;  // per wave (T = 8)
+
+
 constexpr int kMaxTiles = 4;  // distinct tiles per wave
 
 struct WavePairs {
@@ -376,105 +400,114 @@ __device__ __forceinline__ v4i expand16(uint32_t b) {
   return r;
 }
 
+// MFMA shapes for TS-expert tiles.  A and B operands of lane l hold the same
+// k indices, so one expanded fragment serves as both operands of a Gram.
+//   TS = 32: v_mfma_i32_32x32x32_i8, lane l = expert l%32, k-step ks covers
+//            tokens 32*ks + 16*(l/32) .. +15 of the word; C row 8*(r/4)+4*(l/32)+r%4, col l%32
+//   TS = 16: v_mfma_i32_16x16x64_i8, lane l = expert l%16, tokens 16*(l/16) .. +15;
+//            C row 4*(l/16)+r, col l%16
+template <int TS>
+struct Mfma;
+template <>
+struct Mfma<32> {
+  typedef v16i Acc;
+  static constexpr int kSteps = 2, kRegs = 16;
+  __device__ static __forceinline__ int expert(int tile, int lane) { return tile * 32 + (lane & 31); }
+  __device__ static __forceinline__ int chunk16(int ks, int lane) { return ks * 2 + (lane >> 5); }
+  __device__ static __forceinline__ Acc mac(v4i a, v4i b, Acc c) {
+    return __builtin_amdgcn_mfma_i32_32x32x32_i8(a, b, c, 0, 0, 0);
+  }
+  __device__ static __forceinline__ int row(int r, int lane) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
+  __device__ static __forceinline__ int col(int lane) { return lane & 31; }
+};
+template <>
+struct Mfma<16> {
+  typedef v4i Acc;
+  static constexpr int kSteps = 1, kRegs = 4;
+  __device__ static __forceinline__ int expert(int tile, int lane) { return tile * 16 + (lane & 15); }
+  __device__ static __forceinline__ int chunk16(int, int lane) { return lane >> 4; }
+  __device__ static __forceinline__ Acc mac(v4i a, v4i b, Acc c) {
+    return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
+  }
+  __device__ static __forceinline__ int row(int r, int lane) { return 4 * (lane >> 4) + r; }
+  __device__ static __forceinline__ int col(int lane) { return lane & 15; }
+};
+
+// Tile shape for a padded expert count: 32-wide tiles at 256 experts,
+// 16-wide below (8 tiles at 128 experts spread 36 pairs over all 8 waves).
+template <int EPW>
+struct GramShape {
+  static constexpr int TS = EPW >= 256 ? 32 : 16;
+  static constexpr int T = EPW / TS;
+  static constexpr int MP = T == 8 ? 5 : T == 4 ? 2 : 1;  // tile pairs per wave at most
+};
+
 // Accumulate the wave's tile pairs over `nslot` words of the bit tile.
-// Lane l covers expert (32*tile + l%32) and, in k-step ks, tokens
-// 32*ks + 16*(l/32) .. +15 of the word; the same expansion feeds both MFMA
-// operands, so A and B always agree on which token each k index is.
-template <int T, int W>
-__device__ __forceinline__ void mfma_wave(v16i (&acc)[kMaxPairs], const u64* bt, int stride, int nslot, int lane) {
+template <int TS, int T, int W>
+__device__ __forceinline__ void mfma_wave(typename Mfma<TS>::Acc (&acc)[GramShape<T * TS>::MP], const u64* bt,
+                                          int stride, int nslot, int lane) {
   constexpr WavePairs P = PairsOf<T, W>::v;
   if (P.np == 0) return;
-  const int el = lane & 31;
-  const int half = lane >> 5;
-  for (int s = 0; s < nslot; ++s) {
+#pragma unroll 1
+  for (int s = 0; s < nslot; ++s) {  // not unrolled: keeps the fragment registers to one word's worth
     const uint16_t* w16 = reinterpret_cast<const uint16_t*>(bt + s * stride);
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
+    for (int ks = 0; ks < Mfma<TS>::kSteps; ++ks) {
       v4i f[kMaxTiles];
 #pragma unroll
-      for (int t = 0; t < P.nt; ++t) f[t] = expand16(w16[(P.tile[t] * 32 + el) * 4 + ks * 2 + half]);
+      for (int t = 0; t < P.nt; ++t)
+        f[t] = expand16(w16[(Mfma<TS>::expert(P.tile[t], lane) ^ bt_swz(s)) * 4 + Mfma<TS>::chunk16(ks, lane)]);
 #pragma unroll
-      for (int p = 0; p < P.np; ++p)
-        acc[p] = __builtin_amdgcn_mfma_i32_32x32x32_i8(f[P.pa[p]], f[P.pb[p]], acc[p], 0, 0, 0);
+      for (int p = 0; p < P.np; ++p) acc[p] = Mfma<TS>::mac(f[P.pa[p]], f[P.pb[p]], acc[p]);
     }
   }
 }
 
-template <int T, int W>
-__device__ __forceinline__ void mfma_flush(const v16i (&acc)[kMaxPairs], uint32_t* c, int E, int lane) {
+// Add the wave's partial counts into c (upper triangle, integer atomics).
+template <int TS, int T, int W>
+__device__ __forceinline__ void mfma_flush(const typename Mfma<TS>::Acc (&acc)[GramShape<T * TS>::MP], uint32_t* c,
+                                           int E, int lane) {
   constexpr WavePairs P = PairsOf<T, W>::v;
 #pragma unroll
   for (int p = 0; p < P.np; ++p) {
     const int I = P.tile[P.pa[p]], J = P.tile[P.pb[p]];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int gi = 32 * I + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-      const int gj = 32 * J + (lane & 31);
+    for (int r = 0; r < Mfma<TS>::kRegs; ++r) {
+      const int gi = TS * I + Mfma<TS>::row(r, lane);
+      const int gj = TS * J + Mfma<TS>::col(lane);
       const uint32_t v = (uint32_t)acc[p][r];
       if (gi <= gj && gj < E && v) atomicAdd(&c[(int64_t)gi * E + gj], v);
     }
   }
 }
 
-// One Gram step of wave W: accumulate `nslot` words, then, if `flush`, add the
-// partial counts into c (upper triangle, integer atomics) and restart from 0.
-template <int T, int W>
-__device__ __forceinline__ void mfma_step(v16i (&acc)[kMaxPairs], const u64* bt, int stride, int nslot, int lane,
-                                          bool flush, uint32_t* c, int E) {
-  constexpr WavePairs P = PairsOf<T, W>::v;
-  if (P.np == 0) return;
-  mfma_wave<T, W>(acc, bt, stride, nslot, lane);
-  if (flush) {
-    mfma_flush<T, W>(acc, c, E, lane);
-#pragma unroll
-    for (int p = 0; p < P.np; ++p)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[p][r] = 0;
+template <int TS, int T>
+__device__ __forceinline__ void mfma_dispatch(int wave, typename Mfma<TS>::Acc (&acc)[GramShape<T * TS>::MP],
+                                              const u64* bt, int stride, int nslot, int lane) {
+  switch (wave) {
+    case 0: mfma_wave<TS, T, 0>(acc, bt, stride, nslot, lane); break;
+    case 1: mfma_wave<TS, T, 1>(acc, bt, stride, nslot, lane); break;
+    case 2: mfma_wave<TS, T, 2>(acc, bt, stride, nslot, lane); break;
+    case 3: mfma_wave<TS, T, 3>(acc, bt, stride, nslot, lane); break;
+    case 4: mfma_wave<TS, T, 4>(acc, bt, stride, nslot, lane); break;
+    case 5: mfma_wave<TS, T, 5>(acc, bt, stride, nslot, lane); break;
+    case 6: mfma_wave<TS, T, 6>(acc, bt, stride, nslot, lane); break;
+    default: mfma_wave<TS, T, 7>(acc, bt, stride, nslot, lane); break;
   }
 }
 
-template <int T>
-__device__ __forceinline__ void mfma_step_dispatch(int wave, v16i (&acc)[kMaxPairs], const u64* bt, int stride,
-                                                   int nslot, int lane, bool flush, uint32_t* c, int E) {
+template <int TS, int T>
+__device__ __forceinline__ void mfma_flush_dispatch(int wave, const typename Mfma<TS>::Acc (&acc)[GramShape<T * TS>::MP],
+                                                    uint32_t* c, int E, int lane) {
   switch (wave) {
-    case 0: mfma_step<T, 0>(acc, bt, stride, nslot, lane, flush, c, E); break;
-    case 1: mfma_step<T, 1>(acc, bt, stride, nslot, lane, flush, c, E); break;
-    case 2: mfma_step<T, 2>(acc, bt, stride, nslot, lane, flush, c, E); break;
-    case 3: mfma_step<T, 3>(acc, bt, stride, nslot, lane, flush, c, E); break;
-    case 4: mfma_step<T, 4>(acc, bt, stride, nslot, lane, flush, c, E); break;
-    case 5: mfma_step<T, 5>(acc, bt, stride, nslot, lane, flush, c, E); break;
-    case 6: mfma_step<T, 6>(acc, bt, stride, nslot, lane, flush, c, E); break;
-    default: mfma_step<T, 7>(acc, bt, stride, nslot, lane, flush, c, E); break;
-  }
-}
-
-template <int T>
-__device__ __forceinline__ void mfma_dispatch(int wave, v16i (&acc)[kMaxPairs], const u64* bt, int stride, int nslot,
-                                              int lane) {
-  switch (wave) {
-    case 0: mfma_wave<T, 0>(acc, bt, stride, nslot, lane); break;
-    case 1: mfma_wave<T, 1>(acc, bt, stride, nslot, lane); break;
-    case 2: mfma_wave<T, 2>(acc, bt, stride, nslot, lane); break;
-    case 3: mfma_wave<T, 3>(acc, bt, stride, nslot, lane); break;
-    case 4: mfma_wave<T, 4>(acc, bt, stride, nslot, lane); break;
-    case 5: mfma_wave<T, 5>(acc, bt, stride, nslot, lane); break;
-    case 6: mfma_wave<T, 6>(acc, bt, stride, nslot, lane); break;
-    default: mfma_wave<T, 7>(acc, bt, stride, nslot, lane); break;
-  }
-}
-
-template <int T>
-__device__ __forceinline__ void mfma_flush_dispatch(int wave, const v16i (&acc)[kMaxPairs], uint32_t* c, int E,
-                                                    int lane) {
-  switch (wave) {
-    case 0: mfma_flush<T, 0>(acc, c, E, lane); break;
-    case 1: mfma_flush<T, 1>(acc, c, E, lane); break;
-    case 2: mfma_flush<T, 2>(acc, c, E, lane); break;
-    case 3: mfma_flush<T, 3>(acc, c, E, lane); break;
-    case 4: mfma_flush<T, 4>(acc, c, E, lane); break;
-    case 5: mfma_flush<T, 5>(acc, c, E, lane); break;
-    case 6: mfma_flush<T, 6>(acc, c, E, lane); break;
-    default: mfma_flush<T, 7>(acc, c, E, lane); break;
+    case 0: mfma_flush<TS, T, 0>(acc, c, E, lane); break;
+    case 1: mfma_flush<TS, T, 1>(acc, c, E, lane); break;
+    case 2: mfma_flush<TS, T, 2>(acc, c, E, lane); break;
+    case 3: mfma_flush<TS, T, 3>(acc, c, E, lane); break;
+    case 4: mfma_flush<TS, T, 4>(acc, c, E, lane); break;
+    case 5: mfma_flush<TS, T, 5>(acc, c, E, lane); break;
+    case 6: mfma_flush<TS, T, 6>(acc, c, E, lane); break;
+    default: mfma_flush<TS, T, 7>(acc, c, E, lane); break;
   }
 }
 
@@ -483,7 +516,8 @@ __device__ __forceinline__ void mfma_flush_dispatch(int wave, const v16i (&acc)[
 // Per-segment view used by the kernel.
 struct SegView {
   const unsigned char* base;
-  int64_t n, off, w_first, t_begin, t_end;  // t_begin/t_end: the segment's range of global words
+  int64_t n, off, w_first, words;  // words: signature words this segment covers
+  int64_t u_begin, u_end;          // its range of global 8-word units
   int layer;
 };
 
@@ -493,31 +527,36 @@ __device__ __forceinline__ SegView seg_view(const SegTable& tab, int i) {
   v.n = tab.s[i].n;
   v.off = tab.s[i].tok_off;
   v.w_first = v.off >> 6;
-  v.t_begin = tab.tile_start[i];
-  v.t_end = tab.tile_start[i + 1];
+  v.words = v.n > 0 ? ((v.off + v.n - 1) >> 6) - v.w_first + 1 : 0;
+  v.u_begin = tab.tile_start[i];
+  v.u_end = tab.tile_start[i + 1];
   v.layer = tab.s[i].layer;
   return v;
 }
 
-// Segment holding global word g (segments with no words are skipped).
-__device__ __forceinline__ int seg_of(const SegTable& tab, int64_t g, int from) {
+// Segment holding global unit u (segments with no units are skipped).
+__device__ __forceinline__ int seg_of(const SegTable& tab, int64_t u, int from) {
   int i = from;
-  while (i + 1 < tab.nseg && g >= tab.tile_start[i + 1]) ++i;
+  while (i + 1 < tab.nseg && u >= tab.tile_start[i + 1]) ++i;
   return i;
 }
 
+typedef unsigned long long v2u64 __attribute__((ext_vector_type(2)));
+
 // ---------------------------------------------------------------------------
-// Top-K (+ Gram) kernel.  One persistent block per CU slot; block b owns the
-// contiguous range [b*T/G, (b+1)*T/G) of the T global signature words of the
-// launch and walks it 8 words (one per wave) at a time, never mixing two
-// segments in one step.  Gram accumulators are flushed whenever the next step
-// belongs to another layer, and at the end.
-// flags bit 0: fast path allowed (16-byte rows, k <= 8, E <= 256).
+// Top-K (+ Gram) kernel.  Work unit: 8 consecutive signature words (512
+// output positions) of one segment, starting 8-aligned within it; one unit
+// per block step, one word (64 tokens) per wave.  One persistent block per CU
+// slot takes the contiguous unit range [b*U/G, (b+1)*U/G).  Gram
+// accumulators are flushed whenever the next unit belongs to another layer,
+// and at the end.  flags bit 0: fast path allowed (16-byte rows, k <= 8,
+// E <= 256).
 // ---------------------------------------------------------------------------
 template <typename T, int EP, int GM>
 __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab, const PathArgs a, int flags) {
   constexpr int EPW = EP < 32 ? 32 : EP;  // signature words per slot of the bit tile
-  constexpr int NT = EPW / 32;            // 32-expert tiles
+  typedef GramShape<EPW> GS;
+  typedef typename Mfma<GS::TS>::Acc Acc;
   extern __shared__ __align__(16) unsigned char smem[];
   const bool fast = (flags & 1) != 0;
   unsigned char* stage_all = smem;
@@ -530,19 +569,19 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab, cons
   const int nch = (rowv + 7) >> 3;
   unsigned char* st = stage_all + wave * 2 * kChunkBytes;  // this wave's two stage buffers
 
-  const int64_t T_all = tab.tile_start[tab.nseg];
-  const int64_t gs = (int64_t)blockIdx.x * T_all / gridDim.x;
-  const int64_t ge = (int64_t)(blockIdx.x + 1) * T_all / gridDim.x;
-  if (gs >= ge) return;
+  const int64_t U = tab.tile_start[tab.nseg];
+  const int64_t ug = (int64_t)blockIdx.x * U / gridDim.x;
+  const int64_t ue = (int64_t)(blockIdx.x + 1) * U / gridDim.x;
+  if (ug >= ue) return;
 
   PopcGram<EPW, kFusedThreads, GM == kGramPopc> pg;
   if (GM == kGramPopc) pg.init(tid, E);
-  v16i acc[kMaxPairs];
+  Acc acc[GS::MP];
   auto zero_acc = [&]() {
 #pragma unroll
-    for (int p = 0; p < kMaxPairs; ++p)
+    for (int p = 0; p < GS::MP; ++p)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[p][r] = 0;
+      for (int r = 0; r < Mfma<GS::TS>::kRegs; ++r) acc[p][r] = 0;
   };
   zero_acc();
 
@@ -563,14 +602,14 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab, cons
 #pragma unroll
       for (int j = 0; j < 8; ++j)
         __builtin_amdgcn_global_load_lds(cbase + (uint32_t)(j * 8 * rowB) + ((j & 1) ? off_odd : off_even),
-                                         (__attribute__((address_space(3))) void*)(sbuf + j * 1024), 16, 0, 0);
+                                         (__attribute__((address_space(3))) void*)(sbuf + j * 1024), 16, 0, kStreamPolicy);
     } else {
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         const int64_t tr = t0_ + 8 * j + (lane >> 3);
         if (tr >= 0 && tr < sv.n)
           __builtin_amdgcn_global_load_lds(cbase + (uint32_t)(j * 8 * rowB) + ((j & 1) ? off_odd : off_even),
-                                           (__attribute__((address_space(3))) void*)(sbuf + j * 1024), 16, 0, 0);
+                                           (__attribute__((address_space(3))) void*)(sbuf + j * 1024), 16, 0, kStreamPolicy);
       }
     }
   };
@@ -594,135 +633,162 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab, cons
   // bf16 starts with them; an fp32 wave switches after meeting a non-positive threshold.
   bool gen = Traits<T>::kExact;
   int cb = 0;  // stage buffer holding the current chunk
+  const uint32_t vmask = Traits<T>::kExact ? 0xFFFF0000u : 0xFFFFFF00u;  // value bits of a key (VGPR operand of bfi)
 
-  int seg = seg_of(tab, gs, 0);
+  int seg = seg_of(tab, ug, 0);
   SegView sv = seg_view(tab, seg);
-  if (fast && gs + wave < min(ge, sv.t_end)) dma(sv, gs + wave - sv.t_begin, 0, st);
+  {
+    const int64_t tl = 8 * (ug - sv.u_begin) + wave;
+    if (fast && tl < sv.words) dma(sv, tl, 0, st);
+  }
 
   int buf = 0;
-  int64_t p = gs;
-  while (p < ge) {  // one run of steps within one layer, then a flush
-  const int run_layer = sv.layer;
-  for (; p < ge && sv.layer == run_layer; buf ^= 1) {
-    const int64_t cnt = min((int64_t)kFusedWaves, min(ge, sv.t_end) - p);  // words in this step
-    // position and segment of the next step (block-uniform)
-    const int64_t pn = p + cnt;
-    const int seg_n = (pn < ge) ? seg_of(tab, pn, seg) : seg;
-    const SegView svn = seg_view(tab, seg_n);
-    const bool next_mine = pn + wave < min(ge, svn.t_end);
+  int64_t u = ug;
+  while (u < ue) {  // one run of units within one layer, then a flush
+    const int run_layer = sv.layer;
+    for (; u < ue && sv.layer == run_layer; buf ^= 1) {
+      const int64_t tl0 = 8 * (u - sv.u_begin);                  // local word of slot 0
+      const int64_t cnt = min((int64_t)kFusedWaves, sv.words - tl0);  // words in this unit
+      // next unit and its segment (block-uniform)
+      const int64_t un = u + 1;
+      const int seg_n = (un < ue) ? seg_of(tab, un, seg) : seg;
+      const SegView svn = seg_view(tab, seg_n);
+      const int64_t tln = 8 * (un - svn.u_begin) + wave;  // this wave's word in the next unit
+      const bool next_mine = un < ue && tln < svn.words;
 
-    u64* bt = bt_all + buf * kFusedWaves * EPW;
-    u64* mybt = bt + wave * EPW;
+      u64* bt = bt_all + buf * kFusedWaves * EPW;
+      u64* mybt = bt + wave * EPW;
 #pragma unroll
-    for (int e0 = 0; e0 < EPW; e0 += 64)
-      if (e0 + lane < EPW) mybt[e0 + lane] = 0;
-    DOL_WAVE_FENCE();
-    const int64_t tl0 = p - sv.t_begin;  // local word of slot 0
-    if (fast && wave >= cnt && next_mine) {
-      // idle this step (segment end) but busy in the next one, which may lie in
-      // another segment: start that tile's first chunk now, into the buffer the
-      // next step reads first
-      dma(svn, pn + wave - svn.t_begin, 0, st + cb * kChunkBytes);
-    }
-    if (wave < cnt) {
-      const int64_t tl = tl0 + wave;
-      const int64_t t0 = (sv.w_first + tl) * 64 - sv.off;  // token of lane 0 (negative in a history's first partial word)
-      const int64_t t = t0 + lane;
-      const bool valid = (t >= 0) && (t < sv.n);
-      bool need_slow = valid;
-      if (fast) {
-        int top[8];
-        int rej = INT_MIN;
+      for (int e0 = 0; e0 < EPW; e0 += 64)
+        if (e0 + lane < EPW) mybt[e0 + lane] = 0;
+      DOL_WAVE_FENCE();
+      if (fast && wave >= cnt && next_mine) {
+        // idle in this unit (segment end) but busy in the next one: start that
+        // word's first chunk now, into the buffer the next unit reads first
+        dma(svn, tln, 0, st + cb * kChunkBytes);
+      }
+      if (wave < cnt) {
+        const int64_t tl = tl0 + wave;
+        const int64_t t0 = (sv.w_first + tl) * 64 - sv.off;  // token of lane 0 (negative in a history's first partial word)
+        const int64_t t = t0 + lane;
+        const bool valid = (t >= 0) && (t < sv.n);
+        bool need_slow = valid;
+        if (fast) {
+          int top[8];
+          int rej = INT_MIN;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) top[i] = INT_MIN;
-        for (int c = 0; c < nch; ++c) {
-          unsigned char* cur = st + cb * kChunkBytes;
-          if (c * 8 + 8 <= rowv) {
-            DOL_WAIT_VMEM();  // this chunk's direct-to-LDS loads have landed
-          } else {
-            fill_partial(sv, t0, c, cur);
+          for (int i = 0; i < 8; ++i) top[i] = INT_MIN;
+          for (int c = 0; c < nch; ++c) {
+            unsigned char* cur = st + cb * kChunkBytes;
+            if (c * 8 + 8 <= rowv) {
+              DOL_WAIT_VMEM();  // this chunk's direct-to-LDS loads have landed
+            } else {
+              fill_partial(sv, t0, c, cur);
+            }
+            DOL_WAVE_FENCE();
+            unsigned char* other = st + (cb ^ 1) * kChunkBytes;
+            if (c + 1 < nch)
+              dma(sv, tl, c + 1, other);
+            else if (next_mine)
+              dma(svn, tln, 0, other);
+            if (gen)
+              rank_chunk<T, true>(cur, lane, c * 8, vmask, top, rej);
+            else
+              rank_chunk<T, false>(cur, lane, c * 8, vmask, top, rej);
+            DOL_WAVE_FENCE();
+            cb ^= 1;
           }
-          DOL_WAVE_FENCE();
-          unsigned char* other = st + (cb ^ 1) * kChunkBytes;
-          if (c + 1 < nch)
-            dma(sv, tl, c + 1, other);
-          else if (next_mine)
-            dma(svn, pn + wave - svn.t_begin, 0, other);
-          if (gen)
-            rank_chunk<T, true>(cur, lane, c * 8, top, rej);
-          else
-            rank_chunk<T, false>(cur, lane, c * 8, top, rej);
-          DOL_WAVE_FENCE();
-          cb ^= 1;
-        }
-        int sk = INT_MIN, sk1 = rej;
+          int sk = INT_MIN, sk1 = rej;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          sk = (i == k - 1) ? top[i] : sk;
-          sk1 = (i == k) ? top[i] : sk1;
+          for (int i = 0; i < 8; ++i) {
+            sk = (i == k - 1) ? top[i] : sk;
+            sk1 = (i == k) ? top[i] : sk1;
+          }
+          bool ok = top[0] < kCompPosInf;
+          bool nonpos = false;
+          if (gen) {
+            ok = ok && sk > kCompNegInfMax && (sk < Traits<T>::kZeroLo || sk > Traits<T>::kZeroHi);
+          } else {
+            nonpos = valid && sk < Traits<T>::kPosMin;
+            ok = ok && !nonpos;
+          }
+          if (!Traits<T>::kExact) ok = ok && ((sk1 >> 8) < (sk >> 8));
+          need_slow = valid && !ok;
+          if (valid && ok) {
+            const u64 bit = 1ull << lane;
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+              if (i < k) atomicOr(&mybt[(255 - (top[i] & 255)) ^ bt_swz(wave)], bit);
+          }
+          if (__ballot(nonpos) != 0ull) gen = true;
         }
-        bool ok = top[0] < kCompPosInf;
-        bool nonpos = false;
-        if (gen) {
-          ok = ok && sk > kCompNegInfMax && (sk < Traits<T>::kZeroLo || sk > Traits<T>::kZeroHi);
+        if (__ballot(need_slow) != 0ull) {
+          if (need_slow) {
+            const T* row = reinterpret_cast<const T*>(sv.base) + t * (int64_t)E;
+            if (k <= 8)
+              exact_topk8_lane<T>(row, E, k, mybt, bt_swz(wave), 1ull << lane);
+            else
+              exact_topk_passes_lane<T>(row, E, k, mybt, bt_swz(wave), 1ull << lane);
+          }
+        }
+      }
+      __syncthreads();
+      // signatures of the unit's words: pairs of words as 16-byte stores
+      // (8-aligned units make them 16-byte aligned unless the history starts
+      // mid-word), partial history words OR-ed in
+      // One wave per unit (rotating) issues all of the unit's stores, so only
+      // it later waits for their completion in its next vmcnt(0).
+      if (a.bits != nullptr && wave == (int)(u & 7)) {
+        u64* lb = a.bits + (int64_t)sv.layer * a.bits_layer_words;
+        const int64_t w0 = sv.w_first + tl0;
+        auto plain = [&](int s_) {
+          const int64_t t0s = (w0 + s_) * 64 - sv.off;
+          return !a.or_partial || (t0s >= 0 && t0s + 64 <= sv.n);
+        };
+        auto put = [&](int e_, int s_, u64 word) {
+          u64* dst = lb + (int64_t)e_ * a.W + w0 + s_;
+          if (plain(s_))
+            *dst = word;
+          else if (word)
+            atomicOr(dst, word);
+        };
+        if ((w0 & 1) == 0) {
+          for (int item = lane; item < E * 4; item += kWave) {
+            const int e = item >> 2, s0 = (item & 3) * 2;
+            if (s0 >= cnt) continue;
+            const u64 wa = bt[s0 * EPW + (e ^ bt_swz(s0))];
+            const u64 wb = bt[(s0 + 1) * EPW + (e ^ bt_swz(s0 + 1))];
+            if (s0 + 1 < cnt && plain(s0) && plain(s0 + 1)) {
+              *reinterpret_cast<v2u64*>(lb + (int64_t)e * a.W + w0 + s0) = v2u64{wa, wb};
+            } else {
+              put(e, s0, wa);
+              if (s0 + 1 < cnt) put(e, s0 + 1, wb);
+            }
+          }
         } else {
-          nonpos = valid && sk < Traits<T>::kPosMin;
-          ok = ok && !nonpos;
-        }
-        if (!Traits<T>::kExact) ok = ok && ((sk1 >> 8) < (sk >> 8));
-        need_slow = valid && !ok;
-        if (valid && ok) {
-          const u64 bit = 1ull << lane;
-#pragma unroll
-          for (int i = 0; i < 8; ++i)
-            if (i < k) atomicOr(&mybt[255 - (top[i] & 255)], bit);
-        }
-        if (__ballot(nonpos) != 0ull) gen = true;
-      }
-      if (__ballot(need_slow) != 0ull) {
-        if (need_slow) {
-          const T* row = reinterpret_cast<const T*>(sv.base) + t * (int64_t)E;
-          if (k <= 8)
-            exact_topk8_lane<T>(row, E, k, mybt, 1ull << lane);
-          else
-            exact_topk_passes_lane<T>(row, E, k, mybt, 1ull << lane);
+          for (int item = lane; item < E * kFusedWaves; item += kWave) {
+            const int e = item >> 3, s0 = item & 7;
+            if (s0 < cnt) put(e, s0, bt[s0 * EPW + (e ^ bt_swz(s0))]);
+          }
         }
       }
+      if (GM == kGramMfma) mfma_dispatch<GS::TS, GS::T>(wave, acc, bt, EPW, kFusedWaves, lane);  // empty slots are zero
+      if (GM == kGramPopc) pg.accumulate(bt, (int)cnt, EPW);
+      u = un;
+      seg = seg_n;
+      sv = svn;
     }
-    __syncthreads();
-    // signatures: up to 8 consecutive words per expert, written as 64-byte runs
-    if (a.bits != nullptr) {
-      u64* lb = a.bits + (int64_t)sv.layer * a.bits_layer_words;
-      for (int item = tid; item < E * kFusedWaves; item += kFusedThreads) {
-        const int e = item >> 3, s = item & 7;
-        if (s >= cnt) continue;
-        const int64_t w = sv.w_first + tl0 + s;
-        const int64_t t0s = w * 64 - sv.off;
-        const u64 word = bt[s * EPW + e];
-        u64* dst = lb + (int64_t)e * a.W + w;
-        if (!a.or_partial || (t0s >= 0 && t0s + 64 <= sv.n))
-          *dst = word;
-        else if (word)
-          atomicOr(dst, word);
+    if (GM != kGramNone) {
+      uint32_t* cl = a.cacc + (int64_t)run_layer * a.cacc_layer_elems;
+      if (GM == kGramMfma) {
+        mfma_flush_dispatch<GS::TS, GS::T>(wave, acc, cl, E, lane);
+        zero_acc();
+      }
+      if (GM == kGramPopc) {
+        pg.flush(cl, E);
+        pg.init(tid, E);
       }
     }
-    if (GM == kGramMfma) mfma_dispatch<NT>(wave, acc, bt, EPW, kFusedWaves, lane);  // empty slots are zero
-    if (GM == kGramPopc) pg.accumulate(bt, (int)cnt, EPW);
-    p = pn;
-    seg = seg_n;
-    sv = svn;
-  }
-  if (GM != kGramNone) {
-    uint32_t* cl = a.cacc + (int64_t)run_layer * a.cacc_layer_elems;
-    if (GM == kGramMfma) {
-      mfma_flush_dispatch<NT>(wave, acc, cl, E, lane);
-      zero_acc();
-    }
-    if (GM == kGramPopc) {
-      pg.flush(cl, E);
-      pg.init(tid, E);
-    }
-  }
   }
 }
 
@@ -747,8 +813,8 @@ hipError_t launch_one(const SegTable& tab, const PathArgs& a, bool fast, hipStre
   int occ = 1;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kern, kFusedThreads, lds) != hipSuccess || occ < 1) occ = 1;
   const DevInfo di = device_info();
-  const int64_t words = tab.tile_start[tab.nseg];
-  int64_t blocks = std::min<int64_t>((int64_t)di.cu_count * occ, (words + kFusedWaves - 1) / kFusedWaves);
+  const int64_t units = tab.tile_start[tab.nseg];
+  int64_t blocks = std::min<int64_t>((int64_t)di.cu_count * occ, units);
   blocks = std::max<int64_t>(blocks, 1);
   hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kFusedThreads), lds, s, tab, a, fast ? 1 : 0);
   return hipGetLastError();
@@ -782,7 +848,7 @@ hipError_t launch_topk(do_dtype dt, SegTable& tab, int nseg, const PathArgs& a, 
   for (int i = 0; i < nseg; ++i) {
     const int64_t n = tab.s[i].n, off = tab.s[i].tok_off;
     const int64_t words = n > 0 ? ((off + n - 1) >> 6) - (off >> 6) + 1 : 0;
-    tab.tile_start[i + 1] = tab.tile_start[i] + words;
+    tab.tile_start[i + 1] = tab.tile_start[i] + (words + kFusedWaves - 1) / kFusedWaves;  // 8-word units
   }
   if (tab.tile_start[nseg] == 0) return hipSuccess;
   const bool fast = fast_ok && a.k <= kFastMaxK && a.E <= kFastMaxE;
