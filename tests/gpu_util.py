@@ -28,3 +28,43 @@ def loss_close(got: dict, ref: dict, rel: float = 1e-5):
     for f in ("loss", "mean"):
         assert abs(got[f] - ref[f]) <= rel * abs(ref[f]) + 1e-12, (f, got, ref)
     assert abs(got["var"] - ref["var"]) <= rel * abs(ref["var"]) + 1e-9 * max(1.0, ref["mean"] ** 2), (got, ref)
+
+
+def upload_workload(syn, cfg: int, layers: int, keep=()) -> tuple:
+    """Device tensor [layers][N][E] of a synthetic workload, generated one layer at
+    a time on the host; host copies of the layers listed in `keep` are returned too."""
+    w = syn.WORKLOADS[cfg]
+    N, E = w["n"], w["E"]
+    tdt = torch.float32 if w["dtype"] == 0 else torch.bfloat16
+    dev = torch.empty((layers, N, E), dtype=tdt, device="cuda")
+    kept = {}
+    for l in range(layers):
+        x = syn.workload_fill(cfg, l)
+        if l in keep:
+            kept[l] = x
+        t = torch.from_numpy(x) if w["dtype"] == 0 else torch.from_numpy(x.view(np.int16)).view(torch.bfloat16)
+        dev[l].copy_(t)
+    torch.cuda.synchronize()
+    return dev, kept
+
+
+def bits_at(words: np.ndarray, tokens: np.ndarray) -> np.ndarray:
+    """Dense 0/1 [E][len(tokens)] of the signature words [E][W] at the given token positions."""
+    w = words[:, tokens >> 6]
+    return ((w >> (tokens & 63).astype(np.uint64)) & np.uint64(1)).astype(np.uint8)
+
+
+def check_invariants(words: np.ndarray, D: np.ndarray, rec: dict, N: int, k: int, label: str):
+    """Properties that hold at any size (Eq. 2, App. C.2/C.3 row sums, exact loss of D)."""
+    E = D.shape[0]
+    loads = np.bitwise_count(words).sum(axis=1, dtype=np.int64)
+    assert loads.sum() == N * k, f"{label}: {loads.sum()} selections, expected {N * k}"
+    assert np.array_equal(D, D.T), f"{label}: D not symmetric"
+    assert not np.diagonal(D).any(), f"{label}: nonzero diagonal"
+    Di = D.astype(np.int64)
+    assert Di.sum() == 2 * N * k * (E - k), f"{label}: zero-sum identity violated"
+    rows = Di.sum(axis=1)
+    assert np.array_equal(rows, (E - 2 * k) * loads + N * k), f"{label}: row sums differ from (E-2k) n_i + N k"
+    assert rec["sum"] == int(Di.sum())
+    assert rec["sumsq"] == int((Di * Di).sum())  # < 2^63 for every workload here
+    return loads
