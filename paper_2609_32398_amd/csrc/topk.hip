@@ -91,43 +91,24 @@ struct Traits<uint16_t> {
   static constexpr int kZeroLo = -65536, kZeroHi = 65535;
 };
 
-#define DOL_CAS(a, b)          \
-  {                            \
-    const int hi_ = max(a, b); \
-    const int lo_ = min(a, b); \
-    a = hi_;                   \
-    b = lo_;                   \
-  }
-
-// Batcher odd-even merge sort of 8 keys, descending (19 compare-exchanges).
-__device__ __forceinline__ void sort8_desc(int (&g)[8]) {
-  DOL_CAS(g[0], g[1]) DOL_CAS(g[2], g[3]) DOL_CAS(g[4], g[5]) DOL_CAS(g[6], g[7])
-  DOL_CAS(g[0], g[2]) DOL_CAS(g[1], g[3]) DOL_CAS(g[4], g[6]) DOL_CAS(g[5], g[7])
-  DOL_CAS(g[1], g[2]) DOL_CAS(g[5], g[6])
-  DOL_CAS(g[0], g[4]) DOL_CAS(g[1], g[5]) DOL_CAS(g[2], g[6]) DOL_CAS(g[3], g[7])
-  DOL_CAS(g[2], g[4]) DOL_CAS(g[3], g[5])
-  DOL_CAS(g[1], g[2]) DOL_CAS(g[3], g[4]) DOL_CAS(g[5], g[6])
+// Median of three in one instruction (the compiler does not form it from
+// min/max of non-constant operands).
+__device__ __forceinline__ int med3(int a, int b, int c) {
+  int r;
+  asm("v_med3_i32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
 }
 
-// top <- the 8 largest of top and g (both sorted descending); with TRACK,
-// rej <- max(rej, largest key dropped), i.e. the running 9th largest.
+// Insert key x into the descending list top[0..7], dropping the smallest of
+// the nine.  New entry i is x clamped to [old top[i], old top[i-1]].  With
+// TRACK, rej <- max(rej, dropped key), i.e. the running 9th largest, which is
+// again a clamp because rej <= top[7].
 template <bool TRACK>
-__device__ __forceinline__ void merge8(int (&top)[8], const int (&g)[8], int& rej) {
-  int m[8];
+__device__ __forceinline__ void insert8(int (&top)[8], int x, int& rej) {
+  if (TRACK) rej = med3(rej, top[7], x);
 #pragma unroll
-  for (int i = 0; i < 8; ++i) m[i] = max(top[i], g[7 - i]);
-  if (TRACK) {
-    const int r0 = max(min(top[0], g[7]), min(top[1], g[6]));
-    const int r1 = max(min(top[2], g[5]), min(top[3], g[4]));
-    const int r2 = max(min(top[4], g[3]), min(top[5], g[2]));
-    const int r3 = max(min(top[6], g[1]), min(top[7], g[0]));
-    rej = max(max(rej, max(r0, r1)), max(r2, r3));
-  }
-  DOL_CAS(m[0], m[4]) DOL_CAS(m[1], m[5]) DOL_CAS(m[2], m[6]) DOL_CAS(m[3], m[7])
-  DOL_CAS(m[0], m[2]) DOL_CAS(m[1], m[3]) DOL_CAS(m[4], m[6]) DOL_CAS(m[5], m[7])
-  DOL_CAS(m[0], m[1]) DOL_CAS(m[2], m[3]) DOL_CAS(m[4], m[5]) DOL_CAS(m[6], m[7])
-#pragma unroll
-  for (int i = 0; i < 8; ++i) top[i] = m[i];
+  for (int i = 7; i > 0; --i) top[i] = med3(top[i], top[i - 1], x);
+  top[0] = max(top[0], x);
 }
 
 // (x & mask) | (y & ~mask) in one instruction.  Written out because the
@@ -166,19 +147,13 @@ __device__ __forceinline__ void rank_chunk(const unsigned char* sbuf, int lane, 
   auto piece = [&](int q) { return *reinterpret_cast<const v4u*>(row + ((q ^ sw) << 4)); };
   if (Traits<T>::kVec == 4) {
 #pragma unroll
-    for (int gq = 0; gq < 4; ++gq) {
-      int g[8];
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const v4u x = piece(2 * gq + h);
-        const int e0 = (cv0 + 2 * gq + h) * 4;
-        g[4 * h + 0] = key_f32<GEN>(x.x, e0 + 0, vmask);
-        g[4 * h + 1] = key_f32<GEN>(x.y, e0 + 1, vmask);
-        g[4 * h + 2] = key_f32<GEN>(x.z, e0 + 2, vmask);
-        g[4 * h + 3] = key_f32<GEN>(x.w, e0 + 3, vmask);
-      }
-      sort8_desc(g);
-      merge8<!Traits<T>::kExact>(top, g, rej);
+    for (int q = 0; q < 8; ++q) {
+      const v4u x = piece(q);
+      const int e0 = (cv0 + q) * 4;
+      insert8<!Traits<T>::kExact>(top, key_f32<GEN>(x.x, e0 + 0, vmask), rej);
+      insert8<!Traits<T>::kExact>(top, key_f32<GEN>(x.y, e0 + 1, vmask), rej);
+      insert8<!Traits<T>::kExact>(top, key_f32<GEN>(x.z, e0 + 2, vmask), rej);
+      insert8<!Traits<T>::kExact>(top, key_f32<GEN>(x.w, e0 + 3, vmask), rej);
     }
   } else {
 #pragma unroll
@@ -190,8 +165,8 @@ __device__ __forceinline__ void rank_chunk(const unsigned char* sbuf, int lane, 
       key_bf16x2<GEN>(x.y, e0 + 2, vmask, g[2], g[3]);
       key_bf16x2<GEN>(x.z, e0 + 4, vmask, g[4], g[5]);
       key_bf16x2<GEN>(x.w, e0 + 6, vmask, g[6], g[7]);
-      sort8_desc(g);
-      merge8<false>(top, g, rej);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) insert8<false>(top, g[i], rej);
     }
   }
 }
@@ -220,17 +195,26 @@ __device__ __forceinline__ u64 exact_key64(uint32_t bits, int e) {
 
 // Exact Top-k (k <= 8) of one row in a single pass: insertion of unique
 // 64-bit keys (value key, then the complemented index) into a sorted list.
+// The row is read 16 elements at a time so that the loads of a batch are in
+// flight together instead of one memory round trip per element.
 template <typename T>
 __device__ void exact_topk8_lane(const T* row, int E, int k, u64* bt, int swz, u64 bit) {
   u64 lst[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) lst[i] = 0ull;  // every real key is > 0
-  for (int e = 0; e < E; ++e) {
-    const u64 key = exact_key64(elem_bits<T>(row, e), e);
-    if (key <= lst[7]) continue;
+  for (int e0 = 0; e0 < E; e0 += 16) {
+    uint32_t v[16];
 #pragma unroll
-    for (int i = 7; i > 0; --i) lst[i] = max(lst[i], min(lst[i - 1], key));
-    lst[0] = max(lst[0], key);
+    for (int j = 0; j < 16; ++j) v[j] = (e0 + j < E) ? elem_bits<T>(row, e0 + j) : 0u;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      if (e0 + j >= E) break;
+      const u64 key = exact_key64(v[j], e0 + j);
+      if (key <= lst[7]) continue;
+#pragma unroll
+      for (int i = 7; i > 0; --i) lst[i] = max(lst[i], min(lst[i - 1], key));
+      lst[0] = max(lst[0], key);
+    }
   }
 #pragma unroll
   for (int i = 0; i < 8; ++i)
@@ -238,15 +222,22 @@ __device__ void exact_topk8_lane(const T* row, int E, int k, u64* bt, int swz, u
 }
 
 // Exact Top-k for any k: k selection passes, each taking the largest key
-// below the previous one.
+// below the previous one (rows read 16 elements per batch).
 template <typename T>
 __device__ void exact_topk_passes_lane(const T* row, int E, int k, u64* bt, int swz, u64 bit) {
   u64 prev = ~0ull;
   for (int r = 0; r < k; ++r) {
     u64 best = 0;
-    for (int e = 0; e < E; ++e) {
-      const u64 key = exact_key64(elem_bits<T>(row, e), e);
-      if (key < prev && key > best) best = key;
+    for (int e0 = 0; e0 < E; e0 += 16) {
+      uint32_t v[16];
+#pragma unroll
+      for (int j = 0; j < 16; ++j) v[j] = (e0 + j < E) ? elem_bits<T>(row, e0 + j) : 0u;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        if (e0 + j >= E) break;
+        const u64 key = exact_key64(v[j], e0 + j);
+        if (key < prev && key > best) best = key;
+      }
     }
     atomicOr(&bt[(int)(0xFFFFFFFFu - (uint32_t)(best & 0xFFFFFFFFull)) ^ swz], bit);
     prev = best;
@@ -286,9 +277,9 @@ struct PopcGram {
     }
   }
 
-  // bt: nslot signature words per expert, slot-major with `stride` words per slot
-  __device__ __forceinline__ void accumulate(const u64* bt, int nslot, int stride) {
-    for (int s = 0; s < nslot; ++s) {
+  // bt: signature words per expert, slot-major with `stride` words per slot; slots [s0, s1)
+  __device__ __forceinline__ void accumulate(const u64* bt, int s0, int s1, int stride) {
+    for (int s = s0; s < s1; ++s) {
       const u64* w = bt + s * stride;
 #pragma unroll
       for (int q = 0; q < MTQ; ++q) {
@@ -325,70 +316,48 @@ struct PopcGram {
 };
 
 // ---------------------------------------------------------------------------
-// MFMA Gram.  Expert tiles of 32; the tile pairs (I <= J) of the upper
-// triangle are split over the 8 waves so that each wave needs few distinct
-// tiles (each tile costs one bits->bytes expansion per 32 tokens).
+// MFMA Gram.  The upper triangle of c is split into T x T tile pairs (T <= 8
+// tiles of TS experts).  Every wave runs the same code: it owns four local
+// tiles L0..L3 and five pair slots (L0,L0) (L0,L1) (L1,L2) (L0,L2) (L0,L3),
+// each enabled by a bit of `act`.  For T = 8 wave w takes L = (w, w+1, w+3,
+// w+4) mod 8: slot 0..3 then hold the tile pairs at cyclic distance 0, 1, 2
+// and 3 (8 each), and slot 4 of waves 0-3 those at distance 4 (4) -- every
+// one of the 36 pairs exactly once, with 3-4 distinct tiles per wave.
 // ---------------------------------------------------------------------------
-constexpr int kMaxPairs = 5;  // per wave (T = 8)
+constexpr int kGP = 5;  // pair slots per wave
+__device__ __forceinline__ int slot_a(int p) { return p == 2 ? 1 : 0; }
+__device__ __forceinline__ int slot_b(int p) { return p == 0 ? 0 : p == 1 ? 1 : p == 4 ? 3 : 2; }
 
-
-constexpr int kMaxTiles = 4;  // distinct tiles per wave
-
-struct WavePairs {
-  int nt, np;
-  int tile[kMaxTiles];
-  int pa[kMaxPairs], pb[kMaxPairs];  // indices into tile[]
+struct WaveTiles {
+  int tile[4];
+  int act;  // bit p: slot p accumulates a pair of its own
 };
 
-// T = 8 tiles (E <= 256): 36 pairs, 4-5 pairs and 3-4 tiles per wave.
-constexpr WavePairs kPairs8[8] = {
-    {3, 4, {2, 6, 7, 0}, {0, 0, 1, 2}, {1, 2, 2, 2}},        // (2,6)(2,7)(6,7)(7,7)
-    {4, 5, {1, 3, 5, 7}, {0, 0, 1, 1, 2}, {1, 3, 2, 3, 3}},  // (1,3)(1,7)(3,5)(3,7)(5,7)
-    {3, 4, {4, 5, 6, 0}, {0, 0, 1, 1}, {1, 2, 1, 2}},        // (4,5)(4,6)(5,5)(5,6)
-    {4, 4, {0, 2, 3, 4}, {0, 1, 2, 2}, {2, 2, 2, 3}},        // (0,3)(2,3)(3,3)(3,4)
-    {3, 5, {1, 2, 4, 0}, {0, 0, 1, 1, 2}, {1, 2, 1, 2, 2}},  // (1,2)(1,4)(2,2)(2,4)(4,4)
-    {4, 4, {1, 3, 5, 6}, {0, 0, 1, 3}, {2, 3, 3, 3}},        // (1,5)(1,6)(3,6)(6,6)
-    {4, 5, {0, 1, 2, 5}, {0, 0, 0, 1, 2}, {1, 2, 3, 1, 3}},  // (0,1)(0,2)(0,5)(1,1)(2,5)
-    {4, 5, {0, 4, 6, 7}, {0, 0, 0, 0, 1}, {0, 1, 2, 3, 3}},  // (0,0)(0,4)(0,6)(0,7)(4,7)
-};
-// T = 4 tiles (E <= 128): 10 pairs.
-constexpr WavePairs kPairs4[8] = {
-    {2, 2, {2, 3, 0, 0}, {0, 1}, {1, 1}},  // (2,3)(3,3)
-    {2, 2, {1, 3, 0, 0}, {0, 0}, {0, 1}},  // (1,1)(1,3)
-    {2, 2, {0, 1, 0, 0}, {0, 0}, {0, 1}},  // (0,0)(0,1)
-    {2, 2, {0, 2, 0, 0}, {0, 1}, {1, 1}},  // (0,2)(2,2)
-    {2, 1, {0, 3, 0, 0}, {0}, {1}},        // (0,3)
-    {2, 1, {1, 2, 0, 0}, {0}, {1}},        // (1,2)
-    {0, 0, {0, 0, 0, 0}, {0}, {0}},
-    {0, 0, {0, 0, 0, 0}, {0}, {0}},
-};
-// T = 2 tiles (E <= 64): 3 pairs.
-constexpr WavePairs kPairs2[8] = {
-    {1, 1, {0, 0, 0, 0}, {0}, {0}},  // (0,0)
-    {2, 1, {0, 1, 0, 0}, {0}, {1}},  // (0,1)
-    {1, 1, {1, 0, 0, 0}, {0}, {0}},  // (1,1)
-    {0, 0, {0}, {0}, {0}},
-    {0, 0, {0}, {0}, {0}},
-    {0, 0, {0}, {0}, {0}},
-    {0, 0, {0}, {0}, {0}},
-    {0, 0, {0}, {0}, {0}},
-};
-// T = 1 tile (E <= 32).
-constexpr WavePairs kPairs1[8] = {
-    {1, 1, {0, 0, 0, 0}, {0}, {0}},
-    {0, 0, {0}, {0}, {0}},
-    {0, 0, {0}, {0}, {0}},
-    {0, 0, {0}, {0}, {0}},
-    {0, 0, {0}, {0}, {0}},
-    {0, 0, {0}, {0}, {0}},
-    {0, 0, {0}, {0}, {0}},
-    {0, 0, {0}, {0}, {0}},
-};
-
-template <int T, int W>
-struct PairsOf {
-  static constexpr WavePairs v = T == 8 ? kPairs8[W] : T == 4 ? kPairs4[W] : T == 2 ? kPairs2[W] : kPairs1[W];
-};
+__device__ __forceinline__ WaveTiles wave_tiles(int T, int w) {
+  WaveTiles t;
+  if (T == 8) {
+    t.tile[0] = w;
+    t.tile[1] = (w + 1) & 7;
+    t.tile[2] = (w + 3) & 7;
+    t.tile[3] = (w + 4) & 7;
+    t.act = 0xF | (w < 4 ? 0x10 : 0);
+  } else if (T == 4) {  // distances 0, 1 (slots 0, 1) and 2 (slot 3, waves 0-1)
+    t.tile[0] = w & 3;
+    t.tile[1] = (w + 1) & 3;
+    t.tile[2] = (w + 2) & 3;
+    t.tile[3] = w & 3;
+    t.act = w < 4 ? (0x3 | (w < 2 ? 0x8 : 0)) : 0;
+  } else if (T == 2) {
+    t.tile[0] = w & 1;
+    t.tile[1] = (w + 1) & 1;
+    t.tile[2] = t.tile[3] = w & 1;
+    t.act = w == 0 ? 0x3 : w == 1 ? 0x1 : 0;
+  } else {
+    t.tile[0] = t.tile[1] = t.tile[2] = t.tile[3] = 0;
+    t.act = w == 0 ? 0x1 : 0;
+  }
+  return t;
+}
 
 // 16 signature bits -> 16 bytes of 0/1 (byte b = bit b).
 __device__ __forceinline__ v4i expand16(uint32_t b) {
@@ -439,105 +408,90 @@ template <int EPW>
 struct GramShape {
   static constexpr int TS = EPW >= 256 ? 32 : 16;
   static constexpr int T = EPW / TS;
-  static constexpr int MP = T == 8 ? 5 : T == 4 ? 2 : 1;  // tile pairs per wave at most
 };
 
-// Accumulate the wave's tile pairs over `nslot` words of the bit tile.
-template <int TS, int T, int W>
-__device__ __forceinline__ void mfma_wave(typename Mfma<TS>::Acc (&acc)[GramShape<T * TS>::MP], const u64* bt,
-                                          int stride, int nslot, int lane) {
-  constexpr WavePairs P = PairsOf<T, W>::v;
-  if (P.np == 0) return;
+// Accumulate the wave's pair slots over slots [s0, s1) of the bit tile.
+template <int TS>
+__device__ __forceinline__ void mfma_slots(typename Mfma<TS>::Acc (&acc)[kGP], const WaveTiles& wt, const u64* bt,
+                                           int stride, int s0, int s1, int lane) {
+  if (wt.act == 0) return;
+  const bool need[4] = {(wt.act & 0x1B) != 0, (wt.act & 0x6) != 0, (wt.act & 0xC) != 0, (wt.act & 0x10) != 0};
 #pragma unroll 1
-  for (int s = 0; s < nslot; ++s) {  // not unrolled: keeps the fragment registers to one word's worth
+  for (int s = s0; s < s1; ++s) {  // not unrolled: keeps the fragment registers to one word's worth
     const uint16_t* w16 = reinterpret_cast<const uint16_t*>(bt + s * stride);
 #pragma unroll
     for (int ks = 0; ks < Mfma<TS>::kSteps; ++ks) {
-      v4i f[kMaxTiles];
+      v4i f[4];
 #pragma unroll
-      for (int t = 0; t < P.nt; ++t)
-        f[t] = expand16(w16[(Mfma<TS>::expert(P.tile[t], lane) ^ bt_swz(s)) * 4 + Mfma<TS>::chunk16(ks, lane)]);
+      for (int l = 0; l < 4; ++l)
+        f[l] = need[l] ? expand16(w16[(Mfma<TS>::expert(wt.tile[l], lane) ^ bt_swz(s)) * 4 + Mfma<TS>::chunk16(ks, lane)])
+                       : v4i{0, 0, 0, 0};
 #pragma unroll
-      for (int p = 0; p < P.np; ++p) acc[p] = Mfma<TS>::mac(f[P.pa[p]], f[P.pb[p]], acc[p]);
+      for (int p = 0; p < kGP; ++p)
+        if (wt.act & (1 << p)) acc[p] = Mfma<TS>::mac(f[slot_a(p)], f[slot_b(p)], acc[p]);
     }
   }
 }
 
 // Add the wave's partial counts into c (upper triangle, integer atomics).
-template <int TS, int T, int W>
-__device__ __forceinline__ void mfma_flush(const typename Mfma<TS>::Acc (&acc)[GramShape<T * TS>::MP], uint32_t* c,
-                                           int E, int lane) {
-  constexpr WavePairs P = PairsOf<T, W>::v;
+// The lane index is passed through an empty asm statement so that the
+// compiler cannot hoist the addresses of all the atomics out of the unit loop
+// (it would keep them live in registers for the whole kernel).
+template <int TS>
+__device__ __forceinline__ void mfma_flush(const typename Mfma<TS>::Acc (&acc)[kGP], const WaveTiles& wt, uint32_t* c,
+                                           int E, int lane_in) {
+  int lane = lane_in;
+  asm volatile("" : "+v"(lane));
 #pragma unroll
-  for (int p = 0; p < P.np; ++p) {
-    const int I = P.tile[P.pa[p]], J = P.tile[P.pb[p]];
+  for (int p = 0; p < kGP; ++p) {
+    if (!(wt.act & (1 << p))) continue;
+    const int I = wt.tile[slot_a(p)], J = wt.tile[slot_b(p)];
 #pragma unroll
     for (int r = 0; r < Mfma<TS>::kRegs; ++r) {
       const int gi = TS * I + Mfma<TS>::row(r, lane);
       const int gj = TS * J + Mfma<TS>::col(lane);
       const uint32_t v = (uint32_t)acc[p][r];
-      if (gi <= gj && gj < E && v) atomicAdd(&c[(int64_t)gi * E + gj], v);
+      // a diagonal tile pair holds every pair of its experts twice; keep one
+      const bool keep = (I != J || gi <= gj) && gi < E && gj < E && v != 0u;
+      if (keep) atomicAdd(&c[(int64_t)min(gi, gj) * E + max(gi, gj)], v);
     }
-  }
-}
-
-template <int TS, int T>
-__device__ __forceinline__ void mfma_dispatch(int wave, typename Mfma<TS>::Acc (&acc)[GramShape<T * TS>::MP],
-                                              const u64* bt, int stride, int nslot, int lane) {
-  switch (wave) {
-    case 0: mfma_wave<TS, T, 0>(acc, bt, stride, nslot, lane); break;
-    case 1: mfma_wave<TS, T, 1>(acc, bt, stride, nslot, lane); break;
-    case 2: mfma_wave<TS, T, 2>(acc, bt, stride, nslot, lane); break;
-    case 3: mfma_wave<TS, T, 3>(acc, bt, stride, nslot, lane); break;
-    case 4: mfma_wave<TS, T, 4>(acc, bt, stride, nslot, lane); break;
-    case 5: mfma_wave<TS, T, 5>(acc, bt, stride, nslot, lane); break;
-    case 6: mfma_wave<TS, T, 6>(acc, bt, stride, nslot, lane); break;
-    default: mfma_wave<TS, T, 7>(acc, bt, stride, nslot, lane); break;
-  }
-}
-
-template <int TS, int T>
-__device__ __forceinline__ void mfma_flush_dispatch(int wave, const typename Mfma<TS>::Acc (&acc)[GramShape<T * TS>::MP],
-                                                    uint32_t* c, int E, int lane) {
-  switch (wave) {
-    case 0: mfma_flush<TS, T, 0>(acc, c, E, lane); break;
-    case 1: mfma_flush<TS, T, 1>(acc, c, E, lane); break;
-    case 2: mfma_flush<TS, T, 2>(acc, c, E, lane); break;
-    case 3: mfma_flush<TS, T, 3>(acc, c, E, lane); break;
-    case 4: mfma_flush<TS, T, 4>(acc, c, E, lane); break;
-    case 5: mfma_flush<TS, T, 5>(acc, c, E, lane); break;
-    case 6: mfma_flush<TS, T, 6>(acc, c, E, lane); break;
-    default: mfma_flush<TS, T, 7>(acc, c, E, lane); break;
   }
 }
 
 #define DOL_WAVE_FENCE() asm volatile("" ::: "memory")
 
-// Per-segment view used by the kernel.
-struct SegView {
-  const unsigned char* base;
-  int64_t n, off, w_first, words;  // words: signature words this segment covers
-  int64_t u_begin, u_end;          // its range of global 8-word units
+// One segment as the kernel sees it (all values wave-uniform).
+struct Seg {
+  const unsigned char* base;  // scores of its token 0
+  int64_t n;                  // tokens
+  int64_t off;                // bit position of its token 0 in the output rows
+  int64_t w_first;            // first signature word it touches
+  int64_t words;              // signature words it touches
+  int64_t u_begin;            // its first global unit
   int layer;
 };
 
-__device__ __forceinline__ SegView seg_view(const SegTable& tab, int i) {
-  SegView v;
-  v.base = reinterpret_cast<const unsigned char*>(tab.s[i].scores);
-  v.n = tab.s[i].n;
-  v.off = tab.s[i].tok_off;
+// The segment table is read in place from the kernel-argument segment with
+// scalar loads: indexing the by-value argument with a runtime index would make
+// the compiler copy the whole table to private memory first.
+typedef const __attribute__((address_space(4))) SegTable* SegTablePtr;
+
+__device__ __forceinline__ Seg load_seg(SegTablePtr tab, int i) {
+  Seg v;
+  v.base = reinterpret_cast<const unsigned char*>(tab->s[i].scores);
+  v.n = tab->s[i].n;
+  v.off = tab->s[i].tok_off;
   v.w_first = v.off >> 6;
   v.words = v.n > 0 ? ((v.off + v.n - 1) >> 6) - v.w_first + 1 : 0;
-  v.u_begin = tab.tile_start[i];
-  v.u_end = tab.tile_start[i + 1];
-  v.layer = tab.s[i].layer;
+  v.u_begin = tab->tile_start[i];
+  v.layer = tab->s[i].layer;
   return v;
 }
 
 // Segment holding global unit u (segments with no units are skipped).
-__device__ __forceinline__ int seg_of(const SegTable& tab, int64_t u, int from) {
+__device__ __forceinline__ int seg_of(SegTablePtr tab, int64_t u, int from) {
   int i = from;
-  while (i + 1 < tab.nseg && u >= tab.tile_start[i + 1]) ++i;
+  while (i + 1 < tab->nseg && u >= tab->tile_start[i + 1]) ++i;
   return i;
 }
 
@@ -547,39 +501,46 @@ typedef unsigned long long v2u64 __attribute__((ext_vector_type(2)));
 // Top-K (+ Gram) kernel.  Work unit: 8 consecutive signature words (512
 // output positions) of one segment, starting 8-aligned within it; one unit
 // per block step, one word (64 tokens) per wave.  One persistent block per CU
-// slot takes the contiguous unit range [b*U/G, (b+1)*U/G).  Gram
-// accumulators are flushed whenever the next unit belongs to another layer,
-// and at the end.  flags bit 0: fast path allowed (16-byte rows, k <= 8,
-// E <= 256).
+// slot takes the contiguous unit range [b*U/G, (b+1)*U/G).
+//
+// Software pipeline: the signature stores and the Gram of a unit run during
+// the next unit (stores right after its first chunk arrives, one Gram slot
+// after each ranked chunk), so they overlap other waves' ranking instead of
+// following every barrier at once.  Gram accumulators are flushed when the
+// layer changes and at the end.  flags bit 0: fast path allowed (16-byte
+// rows, k <= 8, E <= 256).
 // ---------------------------------------------------------------------------
 template <typename T, int EP, int GM>
-__global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab, const PathArgs a, int flags) {
+__global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, const PathArgs a, int flags) {
+  (void)tab_arg;  // read through `tab` below (it is the first kernel argument)
+  const SegTablePtr tab = (SegTablePtr)__builtin_amdgcn_kernarg_segment_ptr();
   constexpr int EPW = EP < 32 ? 32 : EP;  // signature words per slot of the bit tile
   typedef GramShape<EPW> GS;
   typedef typename Mfma<GS::TS>::Acc Acc;
   extern __shared__ __align__(16) unsigned char smem[];
   const bool fast = (flags & 1) != 0;
-  unsigned char* stage_all = smem;
   u64* bt_all = reinterpret_cast<u64*>(smem + (fast ? kStageBytes : 0));  // [2][kFusedWaves][EPW]
 
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: keeps per-wave control scalar
   const int E = a.E, k = a.k;
   const int rowB = E * (int)sizeof(T);
   const int rowv = rowB >> 4;
   const int nch = (rowv + 7) >> 3;
-  unsigned char* st = stage_all + wave * 2 * kChunkBytes;  // this wave's two stage buffers
+  unsigned char* st = smem + wave * 2 * kChunkBytes;  // this wave's two stage buffers
 
-  const int64_t U = tab.tile_start[tab.nseg];
+  const int64_t U = tab->tile_start[tab->nseg];
   const int64_t ug = (int64_t)blockIdx.x * U / gridDim.x;
   const int64_t ue = (int64_t)(blockIdx.x + 1) * U / gridDim.x;
   if (ug >= ue) return;
 
   PopcGram<EPW, kFusedThreads, GM == kGramPopc> pg;
   if (GM == kGramPopc) pg.init(tid, E);
-  Acc acc[GS::MP];
+  const WaveTiles wt = wave_tiles(GS::T, wave);
+  Acc acc[kGP];
   auto zero_acc = [&]() {
 #pragma unroll
-    for (int p = 0; p < GS::MP; ++p)
+    for (int p = 0; p < kGP; ++p)
 #pragma unroll
       for (int r = 0; r < Mfma<GS::TS>::kRegs; ++r) acc[p][r] = 0;
   };
@@ -592,13 +553,12 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab, cons
   const uint32_t off_even = (uint32_t)((lane >> 3) * rowB + q_even * 16);        // bytes from the chunk's row 0
   const uint32_t off_odd = (uint32_t)((lane >> 3) * rowB + (q_even ^ 1) * 16);  // odd j: piece q_even ^ 1
 
-  // Direct-to-LDS load of a full 64-row x 128-byte chunk of local word `tl` of
-  // segment `sv` (asynchronous; the consumer waits with DOL_WAIT_VMEM).
-  auto dma = [&](const SegView& sv, int64_t tl, int c_, unsigned char* sbuf) {
+  // Direct-to-LDS load of full 128-byte chunk c_ of the 64 rows starting at
+  // token t0_ of segment sg (asynchronous; the consumer waits with DOL_WAIT_VMEM).
+  auto dma = [&](const Seg& sg, int64_t t0_, int c_, unsigned char* sbuf) {
     if (c_ * 8 + 8 > rowv) return;
-    const int64_t t0_ = (sv.w_first + tl) * 64 - sv.off;
-    const unsigned char* cbase = sv.base + t0_ * rowB + c_ * 128;  // row 0 of the chunk (uniform)
-    if (t0_ >= 0 && t0_ + 64 <= sv.n) {  // every row inside the segment
+    const unsigned char* cbase = sg.base + t0_ * rowB + c_ * 128;  // row 0 of the chunk (uniform)
+    if (t0_ >= 0 && t0_ + 64 <= sg.n) {  // every row inside the segment
 #pragma unroll
       for (int j = 0; j < 8; ++j)
         __builtin_amdgcn_global_load_lds(cbase + (uint32_t)(j * 8 * rowB) + ((j & 1) ? off_odd : off_even),
@@ -607,7 +567,7 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab, cons
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         const int64_t tr = t0_ + 8 * j + (lane >> 3);
-        if (tr >= 0 && tr < sv.n)
+        if (tr >= 0 && tr < sg.n)
           __builtin_amdgcn_global_load_lds(cbase + (uint32_t)(j * 8 * rowB) + ((j & 1) ? off_odd : off_even),
                                            (__attribute__((address_space(3))) void*)(sbuf + j * 1024), 16, 0, kStreamPolicy);
       }
@@ -615,17 +575,116 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab, cons
   };
   // Synchronous fill of a partial chunk (the row ends inside it): missing
   // vectors read as all-ones (a NaN), ranked last and never selected on the fast path.
-  auto fill_partial = [&](const SegView& sv, int64_t t0_, int c_, unsigned char* sbuf) {
+  auto fill_partial = [&](const Seg& sg, int64_t t0_, int c_, unsigned char* sbuf) {
     const int cvn = rowv - c_ * 8;
-    const unsigned char* cbase = sv.base + t0_ * rowB + c_ * 128;
+    const unsigned char* cbase = sg.base + t0_ * rowB + c_ * 128;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int64_t tr = t0_ + 8 * j + (lane >> 3);
       const int q = q_even ^ (j & 1);
       v4u val = v4u{~0u, ~0u, ~0u, ~0u};
-      if (q < cvn && tr >= 0 && tr < sv.n)
+      if (q < cvn && tr >= 0 && tr < sg.n)
         val = *reinterpret_cast<const v4u*>(cbase + (uint32_t)(j * 8 * rowB) + ((j & 1) ? off_odd : off_even));
       *reinterpret_cast<v4u*>(sbuf + j * 1024 + lane * 16) = val;
+    }
+  };
+
+  // Tokens whose k-th and (k+1)-th fp32 keys share a 24-bit value bucket
+  // (bit L of tie_mask; B = bucket of sk, need = picks still missing; row0 =
+  // the row of lane 0's token).  For
+  // each, the whole wave loads the token's row (16 bytes per lane, one round
+  // trip), marks the elements of the bucket with a 16-bit sub-key (low 8 value
+  // bits, then the complemented index) and takes the `need` largest across the
+  // wave: by full value, ties to the lower index.
+  auto resolve_ties = [&](u64 tie_mask, int sk_v, int need_v, bool gen_keys, u64* mybt_, const unsigned char* row0) {
+    while (tie_mask != 0ull) {
+      const int L = __builtin_ctzll(tie_mask);
+      tie_mask &= tie_mask - 1;
+      const int B = __builtin_amdgcn_readlane(sk_v, L) >> 8;
+      const int need_l = __builtin_amdgcn_readlane(need_v, L);
+      const unsigned char* row = row0 + (int64_t)L * rowB;
+      const bool has = lane * 16 < rowB;
+      const v4u x = has ? *reinterpret_cast<const v4u*>(row + lane * 16) : v4u{0u, 0u, 0u, 0u};
+      int sub[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        uint32_t u = x[j];
+        if (gen_keys) u ^= (uint32_t)((int32_t)u >> 31) & 0x7FFFFFFFu;
+        const int e = lane * 4 + j;
+        sub[j] = (has && ((int32_t)u >> 8) == B) ? (int)(((u & 0xFFu) << 8) | (uint32_t)(255 - e)) : -1;
+      }
+      for (int r = 0; r < need_l; ++r) {
+        int m = max(max(sub[0], sub[1]), max(sub[2], sub[3]));
+#pragma unroll
+        for (int d = 1; d < kWave; d <<= 1) m = max(m, __shfl_xor(m, d));
+        if (m < 0) break;
+        if (lane == 0) atomicOr(&mybt_[(255 - (m & 255)) ^ bt_swz(wave)], 1ull << L);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) sub[j] = (sub[j] == m) ? -1 : sub[j];
+      }
+    }
+  };
+
+  // The unit whose bit tile is complete and whose stores and Gram are pending.
+  struct Pending {
+    u64* lb;          // bits of its layer (null: no signature output)
+    int64_t w0;       // its first signature word
+    int cnt;          // words in it
+    int layer;
+    int shared_lo;    // slot 0 holds a word shared with the previous segment (OR it in)
+    int shared_hi;    // slot holding a word shared with the next segment, or -1
+  };
+  Pending pend{};
+  bool have_pend = false;
+  // This wave's share of the pending unit's signature stores: experts
+  // [wave*E/8, (wave+1)*E/8), 64 bytes (8 words) per expert as four 16-byte
+  // stores when the unit starts on an even word, else word by word.
+  auto store_share = [&](const u64* pbt) {
+    if (pend.lb == nullptr) return;
+    const int e_lo = (wave * E) >> 3, e_hi = ((wave + 1) * E) >> 3;
+    auto plain = [&](int s_) { return !((s_ == 0 && pend.shared_lo) || s_ == pend.shared_hi); };
+    auto put = [&](int e_, int s_, u64 word) {
+      u64* dst = pend.lb + (int64_t)e_ * a.W + pend.w0 + s_;
+      if (plain(s_))
+        *dst = word;
+      else if (word)
+        atomicOr(dst, word);
+    };
+    if ((pend.w0 & 1) == 0) {
+      for (int item = e_lo * 4 + lane; item < e_hi * 4; item += kWave) {
+        const int e = item >> 2, s0 = (item & 3) * 2;
+        if (s0 >= pend.cnt) continue;
+        const u64 wa = pbt[s0 * EPW + (e ^ bt_swz(s0))];
+        const u64 wb = pbt[(s0 + 1) * EPW + (e ^ bt_swz(s0 + 1))];
+        if (s0 + 1 < pend.cnt && plain(s0) && plain(s0 + 1)) {
+          *reinterpret_cast<v2u64*>(pend.lb + (int64_t)e * a.W + pend.w0 + s0) = v2u64{wa, wb};
+        } else {
+          put(e, s0, wa);
+          if (s0 + 1 < pend.cnt) put(e, s0 + 1, wb);
+        }
+      }
+    } else {
+      for (int item = e_lo * kFusedWaves + lane; item < e_hi * kFusedWaves; item += kWave) {
+        const int e = item >> 3, s0 = item & 7;
+        if (s0 < pend.cnt) put(e, s0, pbt[s0 * EPW + (e ^ bt_swz(s0))]);
+      }
+    }
+  };
+  // Gram of slots [s0, s1) of the pending unit (empty slots are zero).
+  auto gram_slots = [&](const u64* pbt, int s0, int s1) {
+    if (GM == kGramMfma) mfma_slots<GS::TS>(acc, wt, pbt, EPW, s0, s1, lane);
+    if (GM == kGramPopc) pg.accumulate(pbt, s0, min(s1, pend.cnt), EPW);
+  };
+  auto flush = [&](int layer) {
+    if (GM == kGramNone) return;
+    uint32_t* cl = a.cacc + (int64_t)layer * a.cacc_layer_elems;
+    if (GM == kGramMfma) {
+      mfma_flush<GS::TS>(acc, wt, cl, E, lane);
+      zero_acc();
+    }
+    if (GM == kGramPopc) {
+      pg.flush(cl, E);
+      pg.init(tid, E);
     }
   };
 
@@ -636,160 +695,149 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab, cons
   const uint32_t vmask = Traits<T>::kExact ? 0xFFFF0000u : 0xFFFFFF00u;  // value bits of a key (VGPR operand of bfi)
 
   int seg = seg_of(tab, ug, 0);
-  SegView sv = seg_view(tab, seg);
-  {
-    const int64_t tl = 8 * (ug - sv.u_begin) + wave;
-    if (fast && tl < sv.words) dma(sv, tl, 0, st);
-  }
+  Seg sv = load_seg(tab, seg);
+  int64_t tl0 = 8 * (ug - sv.u_begin);                 // local word of slot 0 of the current unit
+  int64_t t0w = (sv.w_first + tl0 + wave) * 64 - sv.off;  // token of lane 0 of this wave's word
+  if (fast && tl0 + wave < sv.words) dma(sv, t0w, 0, st);
 
   int buf = 0;
-  int64_t u = ug;
-  while (u < ue) {  // one run of units within one layer, then a flush
-    const int run_layer = sv.layer;
-    for (; u < ue && sv.layer == run_layer; buf ^= 1) {
-      const int64_t tl0 = 8 * (u - sv.u_begin);                  // local word of slot 0
-      const int64_t cnt = min((int64_t)kFusedWaves, sv.words - tl0);  // words in this unit
-      // next unit and its segment (block-uniform)
-      const int64_t un = u + 1;
-      const int seg_n = (un < ue) ? seg_of(tab, un, seg) : seg;
-      const SegView svn = seg_view(tab, seg_n);
-      const int64_t tln = 8 * (un - svn.u_begin) + wave;  // this wave's word in the next unit
-      const bool next_mine = un < ue && tln < svn.words;
+  for (int64_t u = ug; u < ue; buf ^= 1) {
+    const int cnt = (int)min((int64_t)kFusedWaves, sv.words - tl0);  // words in this unit
+    // next unit and its segment (wave-uniform)
+    const int64_t un = u + 1;
+    int seg_n = seg;
+    Seg svn = sv;
+    int64_t tl0n = tl0 + 8;
+    if (un < ue && un >= tab->tile_start[seg + 1]) {
+      seg_n = seg_of(tab, un, seg);
+      svn = load_seg(tab, seg_n);
+      tl0n = 8 * (un - svn.u_begin);
+    }
+    const bool next_mine = un < ue && tl0n + wave < svn.words;
+    const int64_t t0n = (svn.w_first + tl0n + wave) * 64 - svn.off;
 
-      u64* bt = bt_all + buf * kFusedWaves * EPW;
-      u64* mybt = bt + wave * EPW;
+    u64* bt = bt_all + buf * kFusedWaves * EPW;
+    const u64* pbt = bt_all + (buf ^ 1) * kFusedWaves * EPW;  // the pending unit's tile
+    u64* mybt = bt + wave * EPW;
 #pragma unroll
-      for (int e0 = 0; e0 < EPW; e0 += 64)
-        if (e0 + lane < EPW) mybt[e0 + lane] = 0;
-      DOL_WAVE_FENCE();
-      if (fast && wave >= cnt && next_mine) {
-        // idle in this unit (segment end) but busy in the next one: start that
-        // word's first chunk now, into the buffer the next unit reads first
-        dma(svn, tln, 0, st + cb * kChunkBytes);
-      }
-      if (wave < cnt) {
-        const int64_t tl = tl0 + wave;
-        const int64_t t0 = (sv.w_first + tl) * 64 - sv.off;  // token of lane 0 (negative in a history's first partial word)
-        const int64_t t = t0 + lane;
-        const bool valid = (t >= 0) && (t < sv.n);
-        bool need_slow = valid;
-        if (fast) {
-          int top[8];
-          int rej = INT_MIN;
+    for (int e0 = 0; e0 < EPW; e0 += 64)
+      if (e0 + lane < EPW) mybt[e0 + lane] = 0;
+    DOL_WAVE_FENCE();
+    int gram_done = have_pend ? 0 : kFusedWaves;  // slots of the pending unit already accumulated
+    bool stored = !have_pend;
+    if (fast && wave >= cnt && next_mine) {
+      // idle in this unit (segment end) but busy in the next one: start that
+      // word's first chunk now, into the buffer the next unit reads first
+      dma(svn, t0n, 0, st + cb * kChunkBytes);
+    }
+    if (wave < cnt) {
+      const int64_t t = t0w + lane;
+      const bool valid = (t >= 0) && (t < sv.n);
+      bool need_slow = valid;
+      if (fast) {
+        int top[8];
+        int rej = INT_MIN;
 #pragma unroll
-          for (int i = 0; i < 8; ++i) top[i] = INT_MIN;
-          for (int c = 0; c < nch; ++c) {
-            unsigned char* cur = st + cb * kChunkBytes;
-            if (c * 8 + 8 <= rowv) {
-              DOL_WAIT_VMEM();  // this chunk's direct-to-LDS loads have landed
-            } else {
-              fill_partial(sv, t0, c, cur);
-            }
-            DOL_WAVE_FENCE();
-            unsigned char* other = st + (cb ^ 1) * kChunkBytes;
-            if (c + 1 < nch)
-              dma(sv, tl, c + 1, other);
-            else if (next_mine)
-              dma(svn, tln, 0, other);
-            if (gen)
-              rank_chunk<T, true>(cur, lane, c * 8, vmask, top, rej);
-            else
-              rank_chunk<T, false>(cur, lane, c * 8, vmask, top, rej);
-            DOL_WAVE_FENCE();
-            cb ^= 1;
+        for (int i = 0; i < 8; ++i) top[i] = INT_MIN;
+        for (int c = 0; c < nch; ++c) {
+          unsigned char* cur = st + cb * kChunkBytes;
+          if (c * 8 + 8 <= rowv) {
+            DOL_WAIT_VMEM();  // this chunk's direct-to-LDS loads (and earlier stores) have completed
+          } else {
+            fill_partial(sv, t0w, c, cur);
           }
-          int sk = INT_MIN, sk1 = rej;
+          DOL_WAVE_FENCE();
+          unsigned char* other = st + (cb ^ 1) * kChunkBytes;
+          if (c + 1 < nch)
+            dma(sv, t0w, c + 1, other);
+          else if (next_mine)
+            dma(svn, t0n, 0, other);
+          if (!stored) {
+            store_share(pbt);
+            stored = true;
+          }
+          if (gen)
+            rank_chunk<T, true>(cur, lane, c * 8, vmask, top, rej);
+          else
+            rank_chunk<T, false>(cur, lane, c * 8, vmask, top, rej);
+          if (gram_done < kFusedWaves) {
+            const int s_end = ((c + 1) * kFusedWaves) / nch;
+            gram_slots(pbt, gram_done, s_end);
+            gram_done = s_end;
+          }
+          DOL_WAVE_FENCE();
+          cb ^= 1;
+        }
+        int sk = INT_MIN, sk1 = rej;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          sk = (i == k - 1) ? top[i] : sk;
+          sk1 = (i == k) ? top[i] : sk1;
+        }
+        bool ok = top[0] < kCompPosInf;
+        bool nonpos = false;
+        if (gen) {
+          ok = ok && sk > kCompNegInfMax && (sk < Traits<T>::kZeroLo || sk > Traits<T>::kZeroHi);
+        } else {
+          nonpos = valid && sk < Traits<T>::kPosMin;
+          ok = ok && !nonpos;
+        }
+        // fp32 keys keep 24 value bits: when the k-th and (k+1)-th keys share a
+        // bucket, the experts above the bucket are certain and the rest are
+        // picked from the bucket by resolve_ties
+        const bool tie = !Traits<T>::kExact && valid && ok && ((sk1 >> 8) == (sk >> 8));
+        need_slow = valid && !ok;
+        int need = 0;
+        if (valid && ok) {
+          const u64 bit = 1ull << lane;
 #pragma unroll
           for (int i = 0; i < 8; ++i) {
-            sk = (i == k - 1) ? top[i] : sk;
-            sk1 = (i == k) ? top[i] : sk1;
-          }
-          bool ok = top[0] < kCompPosInf;
-          bool nonpos = false;
-          if (gen) {
-            ok = ok && sk > kCompNegInfMax && (sk < Traits<T>::kZeroLo || sk > Traits<T>::kZeroHi);
-          } else {
-            nonpos = valid && sk < Traits<T>::kPosMin;
-            ok = ok && !nonpos;
-          }
-          if (!Traits<T>::kExact) ok = ok && ((sk1 >> 8) < (sk >> 8));
-          need_slow = valid && !ok;
-          if (valid && ok) {
-            const u64 bit = 1ull << lane;
-#pragma unroll
-            for (int i = 0; i < 8; ++i)
-              if (i < k) atomicOr(&mybt[(255 - (top[i] & 255)) ^ bt_swz(wave)], bit);
-          }
-          if (__ballot(nonpos) != 0ull) gen = true;
-        }
-        if (__ballot(need_slow) != 0ull) {
-          if (need_slow) {
-            const T* row = reinterpret_cast<const T*>(sv.base) + t * (int64_t)E;
-            if (k <= 8)
-              exact_topk8_lane<T>(row, E, k, mybt, bt_swz(wave), 1ull << lane);
-            else
-              exact_topk_passes_lane<T>(row, E, k, mybt, bt_swz(wave), 1ull << lane);
-          }
-        }
-      }
-      __syncthreads();
-      // signatures of the unit's words: pairs of words as 16-byte stores
-      // (8-aligned units make them 16-byte aligned unless the history starts
-      // mid-word), partial history words OR-ed in
-      // One wave per unit (rotating) issues all of the unit's stores, so only
-      // it later waits for their completion in its next vmcnt(0).
-      if (a.bits != nullptr && wave == (int)(u & 7)) {
-        u64* lb = a.bits + (int64_t)sv.layer * a.bits_layer_words;
-        const int64_t w0 = sv.w_first + tl0;
-        auto plain = [&](int s_) {
-          const int64_t t0s = (w0 + s_) * 64 - sv.off;
-          return !a.or_partial || (t0s >= 0 && t0s + 64 <= sv.n);
-        };
-        auto put = [&](int e_, int s_, u64 word) {
-          u64* dst = lb + (int64_t)e_ * a.W + w0 + s_;
-          if (plain(s_))
-            *dst = word;
-          else if (word)
-            atomicOr(dst, word);
-        };
-        if ((w0 & 1) == 0) {
-          for (int item = lane; item < E * 4; item += kWave) {
-            const int e = item >> 2, s0 = (item & 3) * 2;
-            if (s0 >= cnt) continue;
-            const u64 wa = bt[s0 * EPW + (e ^ bt_swz(s0))];
-            const u64 wb = bt[(s0 + 1) * EPW + (e ^ bt_swz(s0 + 1))];
-            if (s0 + 1 < cnt && plain(s0) && plain(s0 + 1)) {
-              *reinterpret_cast<v2u64*>(lb + (int64_t)e * a.W + w0 + s0) = v2u64{wa, wb};
-            } else {
-              put(e, s0, wa);
-              if (s0 + 1 < cnt) put(e, s0 + 1, wb);
+            if (i < k) {
+              if (!tie || (top[i] >> 8) > (sk >> 8))
+                atomicOr(&mybt[(255 - (top[i] & 255)) ^ bt_swz(wave)], bit);
+              else
+                ++need;
             }
           }
-        } else {
-          for (int item = lane; item < E * kFusedWaves; item += kWave) {
-            const int e = item >> 3, s0 = item & 7;
-            if (s0 < cnt) put(e, s0, bt[s0 * EPW + (e ^ bt_swz(s0))]);
-          }
+        }
+        if (!Traits<T>::kExact) {
+          const u64 tm = __ballot(tie);
+          if (tm != 0ull) resolve_ties(tm, sk, need, gen, mybt, sv.base + t0w * rowB);
+        }
+        if (__ballot(nonpos) != 0ull) gen = true;
+      }
+      if (__ballot(need_slow) != 0ull) {
+        if (need_slow) {
+          const T* row = reinterpret_cast<const T*>(sv.base) + t * (int64_t)E;
+          if (k <= 8)
+            exact_topk8_lane<T>(row, E, k, mybt, bt_swz(wave), 1ull << lane);
+          else
+            exact_topk_passes_lane<T>(row, E, k, mybt, bt_swz(wave), 1ull << lane);
         }
       }
-      if (GM == kGramMfma) mfma_dispatch<GS::TS, GS::T>(wave, acc, bt, EPW, kFusedWaves, lane);  // empty slots are zero
-      if (GM == kGramPopc) pg.accumulate(bt, (int)cnt, EPW);
-      u = un;
-      seg = seg_n;
-      sv = svn;
     }
-    if (GM != kGramNone) {
-      uint32_t* cl = a.cacc + (int64_t)run_layer * a.cacc_layer_elems;
-      if (GM == kGramMfma) {
-        mfma_flush_dispatch<GS::TS, GS::T>(wave, acc, cl, E, lane);
-        zero_acc();
-      }
-      if (GM == kGramPopc) {
-        pg.flush(cl, E);
-        pg.init(tid, E);
-      }
-    }
+    // waves without a fast chunk loop in this unit finish the pending unit here
+    if (!stored) store_share(pbt);
+    if (gram_done < kFusedWaves) gram_slots(pbt, gram_done, kFusedWaves);
+    __syncthreads();  // this unit's bit tile is complete; the pending unit's tile is free
+    if (have_pend && pend.layer != sv.layer) flush(pend.layer);
+    pend.lb = a.bits != nullptr ? a.bits + (int64_t)sv.layer * a.bits_layer_words : nullptr;
+    pend.w0 = sv.w_first + tl0;
+    pend.cnt = cnt;
+    pend.layer = sv.layer;
+    pend.shared_lo = a.or_partial && tl0 == 0 && (sv.off & 63) != 0;
+    pend.shared_hi = (a.or_partial && tl0 + cnt == sv.words && ((sv.off + sv.n) & 63) != 0) ? cnt - 1 : -1;
+    have_pend = true;
+    u = un;
+    seg = seg_n;
+    sv = svn;
+    tl0 = tl0n;
+    t0w = t0n;
   }
+  // the last unit
+  store_share(bt_all + (buf ^ 1) * kFusedWaves * EPW);
+  gram_slots(bt_all + (buf ^ 1) * kFusedWaves * EPW, 0, kFusedWaves);
+  flush(pend.layer);
 }
 
 int g_gram_mode = -1;  // kGramPopc or kGramMfma; read once from DOLOSS_GRAM ("popc" selects popcount)

@@ -146,6 +146,37 @@ def test_negative_and_bucket_ties_fp32(dl, orc, syn, dtype):
         _run_all_entry_points(dl, orc, bits.view(np.float32), 5, "bucket ties")
 
 
+def _bucket_tie_rows(rng, N, E, k, sign):
+    """fp32 rows whose k-th and (k+1)-th largest values share their top 24
+    bits: a cluster of 2..k+3 values b with random low bytes (some exactly
+    equal) sits at random positions among clearly larger and smaller values."""
+    x = rng.normal(size=(N, E)).astype(np.float32)
+    for t in range(N):
+        above = rng.integers(0, k)  # values clearly above the cluster
+        m = int(rng.integers(max(2, k - above + 1), k - above + 4))
+        m = min(m, E - above)
+        pos = rng.permutation(E)
+        b = np.float32(sign * rng.uniform(0.5, 4.0))
+        bb = np.uint32(b.view(np.uint32)) & np.uint32(0xFFFFFF00)
+        low = rng.integers(0, 256, size=m).astype(np.uint32)
+        if m >= 3:
+            low[1] = low[2]  # an exact duplicate inside the bucket
+        cl = (bb | low).view(np.float32)
+        x[t, pos[:m]] = cl
+        x[t, pos[m:m + above]] = np.abs(b) * 4 + 1 + rng.random(above).astype(np.float32)
+        x[t, pos[m + above:]] = -np.abs(b) * 4 - 1 - rng.random(E - m - above).astype(np.float32)
+    return x
+
+
+@pytest.mark.parametrize("E,k", [(32, 1), (32, 5), (100, 8), (256, 8), (256, 3)])
+@pytest.mark.parametrize("sign", [1.0, -1.0])
+def test_fp32_bucket_ties_resolved(dl, orc, E, k, sign):
+    # keys keep 24 value bits: the low 8 bits must still decide the Top-K
+    rng = np.random.default_rng(1000 + E + k)
+    x = _bucket_tie_rows(rng, 700, E, k, sign)
+    _run_all_entry_points(dl, orc, x, k, f"bucket cluster E={E} k={k} sign={sign}")
+
+
 def test_misaligned_scores_take_the_exact_path(dl, orc, syn):
     N, E, k = 500, 64, 6
     x = syn.normal(3, N, E, 0)
