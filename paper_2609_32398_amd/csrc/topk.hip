@@ -12,8 +12,8 @@
 // chunks so the global loads are fully coalesced; the next chunk's loads are
 // issued before the current chunk is ranked, so each wave keeps one chunk in
 // flight at all times.  The 8 signature words of a step land in an LDS tile
-// (double-buffered) from which the block writes them out as 64-byte runs and
-// feeds the Gram.
+// (double-buffered) from which, during the next step, the block writes them
+// out as 64-byte runs per expert and feeds the Gram.
 //
 // Exact Top-K with composite 32-bit keys.  Each element becomes one signed
 // integer whose high bits order the score and whose low byte is (255 - expert
@@ -21,19 +21,20 @@
 // "Positive" keys use the raw bit pattern (one instruction, exact whenever the
 // k-th score is a positive number); "general" keys first map the pattern to
 // an order-preserving integer (exact for all non-NaN values except that -0
-// sorts one step below +0).  bf16 keeps all 16 value bits; fp32 keeps 24, so
-// a token is re-ranked exactly when its k-th and (k+1)-th keys share a 24-bit
-// bucket.  Any token whose threshold lands on +-0, +-inf, NaN or a bucket tie,
-// or whose threshold is not positive under positive keys, is re-ranked by an
-// exact per-lane fallback on 64-bit keys.  bf16 always uses general keys (they
-// cost it little); an fp32 wave starts with positive keys and switches to
-// general keys for the rest of its tiles after meeting a non-positive threshold.
+// sorts one step below +0).  An fp32 wave starts with positive keys and
+// switches to general keys for the rest of its tiles after meeting a
+// non-positive threshold; bf16 waves use general keys throughout.  bf16 keys keep all 16 value bits; fp32 keys keep 24, so a token
+// whose k-th and (k+1)-th keys share a 24-bit bucket is settled by the whole
+// wave from the full values of that bucket.  A token whose threshold lands on
+// +-0, +-inf or NaN, or is not positive under positive keys, is re-ranked by
+// an exact per-lane fallback on 64-bit keys.
 //
-// Gram.  mode 2 (default): int8 MFMA 32x32x32 on 0/1 bytes expanded from the
-// signature words, one or more 32x32 expert tile pairs per wave, accumulators
-// in registers for the whole kernel.  mode 1: VALU popcount(a & b) on 4x4
-// micro-tiles per thread.  Either way each block adds its integer partial
-// counts into the accumulator matrix once at the end (order-independent).
+// Gram.  mode 2 (default): int8 MFMA (32x32x32 at 256 experts, 16x16x64
+// below) on 0/1 bytes expanded from the signature words, up to five expert
+// tile pairs per wave, accumulators in registers.  mode 1: VALU
+// popcount(a & b) on 4x4 micro-tiles per thread.  Either way a block adds its
+// integer partial counts into the accumulator matrix when the layer changes
+// and at the end (order-independent).
 #include <cstdlib>
 
 #include "common.h"
@@ -688,8 +689,11 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
     }
   };
 
-  // General keys cost bf16 ~0.75 extra instructions per score and fp32 ~3, so
-  // bf16 starts with them; an fp32 wave switches after meeting a non-positive threshold.
+  // fp32 waves start with positive keys (general keys cost ~3 more
+  // instructions per score) and switch for the rest of the kernel after
+  // meeting a non-positive threshold; bf16 general keys cost ~1 more per
+  // score, less than the exact re-rank a first non-positive threshold costs
+  // in a short launch, so bf16 starts with them.
   bool gen = Traits<T>::kExact;
   int cb = 0;  // stage buffer holding the current chunk
   const uint32_t vmask = Traits<T>::kExact ? 0xFFFF0000u : 0xFFFFFF00u;  // value bits of a key (VGPR operand of bfi)
