@@ -12,6 +12,9 @@ computes, written from the paper's definitions (arXiv 2609.32398):
 * ``loss``            -- Eq. (3) sum_{i!=j} G_ij^2 (fp64 and exact integer),
   with mean and population variance of the off-diagonal distances
   (App. C.1).
+* ``surrogate``       -- Sec. 3.1.3, Eq. (6)-(7): the surrogate loss
+  (scale/(N^2 k)) sum_ij G_ij C_ij, C_ij = sum_t p_it (f_it - f_jt), and its
+  gradient with respect to the routing probabilities (G, F detached).
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 ``bench.py`` may use this package.  It shares no code with the HIP library.
@@ -60,7 +63,9 @@ def _load():
         lib.oracle_pack.argtypes = [vp, i64, i32, vp]
         lib.oracle_hamming.argtypes = [vp, i64, i32, vp, ctypes.c_int]
         lib.oracle_loss.argtypes = [vp, i32, ctypes.POINTER(_LossResult)]
-        for f in ("oracle_topk_signature", "oracle_pack", "oracle_hamming", "oracle_loss"):
+        lib.oracle_surrogate.argtypes = [vp, ctypes.c_int, i64, i32, i32, vp, vp, ctypes.c_double,
+                                         ctypes.POINTER(ctypes.c_double), vp, ctypes.c_int]
+        for f in ("oracle_topk_signature", "oracle_pack", "oracle_hamming", "oracle_loss", "oracle_surrogate"):
             getattr(lib, f).restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -123,6 +128,24 @@ def loss(D: np.ndarray) -> dict:
     r = _LossResult()
     _load().oracle_loss(D.ctypes.data, E, ctypes.byref(r))
     return dict(sum=int(r.sum), sumsq=int(r.sumsq), loss=float(r.loss), mean=float(r.mean), var=float(r.var))
+
+
+def surrogate(p: np.ndarray, F: np.ndarray, G: np.ndarray, k: int, scale: float = 1.0, want_grad: bool = True,
+              nthreads: int | None = None):
+    """Eq. (7) loss and dL/dp (G, F detached) for p of shape (N, E) (float32 or
+    bf16 bit patterns), F[E][N] 0/1 and G[E][E].  Returns (loss, grad or None)."""
+    p = np.ascontiguousarray(p)
+    N, E = p.shape
+    F = np.ascontiguousarray(F, dtype=np.uint8)
+    G = np.ascontiguousarray(G, dtype=np.uint32)
+    assert F.shape == (E, N) and G.shape == (E, E)
+    grad = np.empty((N, E), dtype=np.float64) if want_grad else None
+    loss = ctypes.c_double()
+    rc = _load().oracle_surrogate(p.ctypes.data, _dtype_of(p), N, E, k, F.ctypes.data, G.ctypes.data, scale,
+                                  ctypes.byref(loss), grad.ctypes.data if want_grad else None, nthreads or threads())
+    if rc:
+        raise ValueError(f"oracle_surrogate: bad arguments N={N} E={E} k={k}")
+    return float(loss.value), grad
 
 
 def run(scores: np.ndarray, k: int, nthreads: int | None = None):

@@ -22,6 +22,11 @@
  *                          distances (Sec. 3.1.1 / App. C.1: minimising the sum
  *                          of squares under the fixed total is minimising the
  *                          variance).  fp64 accumulation, plus exact u64 sums.
+ *   oracle_surrogate       Sec. 3.1.3, Eq. (6)-(7): the surrogate loss
+ *                          (1/(N^2 k)) sum_ij G_ij C_ij with the direction term
+ *                          C_ij = sum_t p_it (f_it - f_jt) written out, and its
+ *                          gradient with respect to the routing probabilities
+ *                          p with G and F held constant.
  *
  * Readings where the paper is silent (each listed in the design notes):
  *   - ties in Top-K go to the lower expert index;
@@ -157,5 +162,47 @@ int oracle_loss(const uint32_t* D, int32_t E, oracle_loss_result* out) {
   out->loss = f2;
   out->mean = mean;
   out->var = acc / P;
+  return 0;
+}
+
+/*
+ * Sec. 3.1.3, Eq. (6)-(7), surrogate loss with the magnitude G detached:
+ *   C_ij = sum_t p_it (f_it - f_jt)
+ *   L    = scale / (N^2 k) * sum_{i,j} G_ij C_ij
+ *   dL/dp_it = scale / (N^2 k) * sum_j G_ij (f_it - f_jt)
+ * p[N][E] (dtype as the scores), F[E][N] 0/1, G[E][E].  `scale` multiplies G
+ * (1 on one device; Sec. 3.1.4 averages G over the data-parallel ranks).
+ * grad (nullable) is [N][E].  Both quantities are evaluated from their
+ * definitions, each with its own loop.
+ */
+int oracle_surrogate(const void* p, int dtype, int64_t N, int32_t E, int32_t k, const uint8_t* F, const uint32_t* G,
+                     double scale, double* loss, double* grad, int nthreads) {
+  if (N < 1 || E < 1 || k < 1 || k > E) return -1;
+  const double norm = scale / ((double)N * (double)N * (double)k);
+  double* C = (double*)calloc((size_t)E * (size_t)E, sizeof(double));
+  if (!C) return -2;
+#pragma omp parallel for schedule(dynamic, 1) num_threads(nthreads > 0 ? nthreads : 1)
+  for (int32_t i = 0; i < E; ++i)
+    for (int32_t j = 0; j < E; ++j) {
+      double c = 0.0;
+      for (int64_t t = 0; t < N; ++t)
+        c += score_at(p, dtype, t * E + i) * ((double)F[(int64_t)i * N + t] - (double)F[(int64_t)j * N + t]);
+      C[(int64_t)i * E + j] = c;
+    }
+  double acc = 0.0;
+  for (int32_t i = 0; i < E; ++i)
+    for (int32_t j = 0; j < E; ++j) acc += (double)G[(int64_t)i * E + j] * C[(int64_t)i * E + j];
+  *loss = norm * acc;
+  free(C);
+  if (grad) {
+#pragma omp parallel for schedule(static) num_threads(nthreads > 0 ? nthreads : 1)
+    for (int64_t t = 0; t < N; ++t)
+      for (int32_t i = 0; i < E; ++i) {
+        double g = 0.0;
+        for (int32_t j = 0; j < E; ++j)
+          g += (double)G[(int64_t)i * E + j] * ((double)F[(int64_t)i * N + t] - (double)F[(int64_t)j * N + t]);
+        grad[t * E + i] = norm * g;
+      }
+  }
   return 0;
 }
