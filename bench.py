@@ -207,6 +207,26 @@ def bench_layers(args, cfg):
     torch.cuda.synchronize()
     nb_ms = sum(a.elapsed_time(b) for a, b in nb) / len(nb)
     nb_bytes = tokens * E * elem
+    # the surrogate loss (Eq. 7) and its gradient on the same tokens: the scores
+    # of this workload are per-token probabilities; signatures and distances
+    # from the headline pass
+    dl.do_fused(scores, k, bits=bits, D=D, out=out)
+    sloss = torch.empty(L, dtype=torch.float64, device=scores.device)
+    sgrad = torch.empty((L, N, E), dtype=torch.float32, device=scores.device)
+    dl.do_surrogate(scores, k, bits, D, loss=sloss, grad=sgrad)
+    torch.cuda.synchronize()
+    sv = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    for a, b in sv:
+        a.record()
+        b.record()
+    torch.cuda.synchronize()
+    for a, b in sv:
+        dl.do_profile_next(a, b)
+        dl.do_surrogate(scores, k, bits, D, loss=sloss, grad=sgrad)
+    torch.cuda.synchronize()
+    s_ms = sum(a.elapsed_time(b) for a, b in sv) / len(sv)
+    s_bytes = tokens * (2 * E * 4 + E // 8) if w["dtype"] == 0 else tokens * (E * 2 + E * 4 + E // 8)
+    del sgrad
     res = dict(
         metric="DO-loss tokens/s per layer (top-k→signature→E×E Hamming→loss); % of HBM peak",
         value=tokens / (ms_per_step / 1e3),
@@ -228,6 +248,10 @@ def bench_layers(args, cfg):
         without_signature_output=dict(kernel_ms=nb_ms, algorithmic_bytes=nb_bytes,
                                       achieved_gbs=nb_bytes / (nb_ms / 1e3) / 1e9,
                                       frac=nb_bytes / (nb_ms / 1e3) / 1e9 / HBM_PEAK_GBS),
+        surrogate=dict(kernel="k_surrogate (Eq. 7 loss and dloss/dp)", kernel_ms=s_ms, algorithmic_bytes=s_bytes,
+                       bytes_per_token=s_bytes // tokens, achieved_gbs=s_bytes / (s_ms / 1e3) / 1e9,
+                       frac=s_bytes / (s_ms / 1e3) / 1e9 / HBM_PEAK_GBS,
+                       tokens_per_s=tokens / (s_ms / 1e3)),
         wall_s_timed=wall,
         check=dict(layer0_sum=rec[0]["sum"], expected_sum=2 * N * k * (E - k)),
     )

@@ -115,6 +115,28 @@ do_status do_fused(const void* scores, do_dtype dtype, int64_t N, int32_t E, int
                    uint32_t* D, do_loss_result* out, hipStream_t stream);
 
 /*
+ * Surrogate DO-loss (Sec. 3.1.3, Eq. 6-7) and its gradient with respect to the
+ * routing probabilities, with the magnitude G and the assignments F detached
+ * (stop-gradient, Sec. 3.1.2):
+ *   C_ij = sum_t p_it (f_it - f_jt)
+ *   loss = scale / (N^2 k) * sum_{i,j} G_ij C_ij
+ *   grad_it = dloss/dp_it = scale / (N^2 k) * sum_j G_ij (f_it - f_jt)
+ * G is `D`; scale is 1 on one device (Sec. 3.1.4: with G summed over R
+ * data-parallel ranks, scale = 1/R gives the averaged magnitude of Eq. 8).
+ *   p     [L][N][E] device, fp32 or bf16 routing probabilities (as given),
+ *         aligned to two elements
+ *   bits  [L][E][ceil(N/64)] device: the tokens' signatures (f_it = bit)
+ *   D     [L][E][E] device
+ *   loss  [L] device doubles, overwritten
+ *   grad  nullable, [L][N][E] device fp32 (8-byte aligned), overwritten
+ * Limits: E <= 256 and (E-1)*N < 2^31 (DO_ERR_OVERFLOW otherwise).  The loss
+ * is accumulated in fp64 with atomic adds, so its last bits may differ
+ * between runs; the gradient is deterministic.
+ */
+do_status do_surrogate(const void* p, do_dtype dtype, int64_t N, int32_t E, int32_t k, int32_t L, const uint64_t* bits,
+                       const uint32_t* D, double scale, double* loss, float* grad, hipStream_t stream);
+
+/*
  * Streaming global-batch history (Sec. 3.1.4: distances over a batch wider
  * than one micro-batch; App. F.2, Table 4: G over gradient-accumulated
  * micro-batches).  A handle owns a

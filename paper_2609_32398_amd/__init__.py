@@ -11,6 +11,7 @@ Functions keep the C names:
 * ``do_pairwise_hamming(bits, N)``   -> D     [L][E][E] int32 (uint32 values)
 * ``do_loss(D)``                     -> out   [L][5] (sum, sumsq, loss, mean, var) as a dict list
 * ``do_fused(scores, k, want_bits)`` -> (bits or None, D, out)
+* ``do_surrogate(p, k, bits, D)``    -> (loss [L] float64, dloss/dp [L][N][E] float32)
 * ``DoStream``                       -> streaming history (do_stream_*)
 
 ``scores`` is a CUDA tensor of shape [N, E] or [L, N, E], float32 or bfloat16.
@@ -54,6 +55,7 @@ def lib():
             "do_pairwise_hamming": ([vp, i64, i32, i32, vp, vp], st),
             "do_loss": ([vp, i32, i32, vp, vp], st),
             "do_fused": ([vp, st, i64, i32, i32, i32, vp, vp, vp, vp], st),
+            "do_surrogate": ([vp, st, i64, i32, i32, i32, vp, vp, ctypes.c_double, vp, vp, vp], st),
             "do_stream_create": ([i32, i32, i64, ctypes.POINTER(vp)], st),
             "do_stream_append": ([vp, vp, st, i64, vp], st),
             "do_stream_append_many": ([vp, ctypes.POINTER(vp), st, i64, i32, vp], st),
@@ -185,6 +187,20 @@ def do_fused(scores: torch.Tensor, k: int, want_bits: bool = False, bits: torch.
                           bits.data_ptr() if bits is not None else None, D.data_ptr(), out.data_ptr(), _stream()),
            "do_fused")
     return bits, D, out
+
+
+def do_surrogate(p: torch.Tensor, k: int, bits: torch.Tensor, D: torch.Tensor, scale: float = 1.0,
+                 want_grad: bool = True, loss: torch.Tensor | None = None, grad: torch.Tensor | None = None):
+    """Eq. (7) surrogate loss per layer (float64 [L]) and dloss/dp (float32 [L, N, E] or None)."""
+    L, N, E = _scores_3d(p)
+    if loss is None:
+        loss = torch.empty(L, dtype=torch.float64, device=p.device)
+    if want_grad and grad is None:
+        grad = torch.empty((L, N, E), dtype=torch.float32, device=p.device)
+    _check(lib().do_surrogate(p.data_ptr(), _dtype_code(p), N, E, k, L, bits.data_ptr(), D.data_ptr(), float(scale),
+                              loss.data_ptr(), grad.data_ptr() if grad is not None else None, _stream()),
+           "do_surrogate")
+    return loss, grad
 
 
 def do_profile_next(start: "torch.cuda.Event | None", stop: "torch.cuda.Event | None"):

@@ -196,6 +196,38 @@ DOLOSS_API do_status do_fused(const void* scores, do_dtype dtype, int64_t N, int
   return hip_status(dol::launch_finalize(D, D, out, E, L, stream), "finalize");
 }
 
+DOLOSS_API do_status do_surrogate(const void* p, do_dtype dtype, int64_t N, int32_t E, int32_t k, int32_t L,
+                                  const uint64_t* bits, const uint32_t* D, double scale, double* loss, float* grad,
+                                  hipStream_t stream) {
+  DO_TRY(check_dtype(dtype));
+  DO_TRY(check_shape(N, E, L));
+  DO_TRY(check_k(k, E));
+  if (E > dol::kFastMaxE) return fail(DO_ERR_INVALID_ARG, "do_surrogate supports E <= 256");
+  if ((int64_t)(E - 1) * N >= (int64_t(1) << 31))
+    return fail(DO_ERR_OVERFLOW, "(E-1)*N must be < 2^31 (row sums of G are int32)");
+  if (p == nullptr || !aligned(p, 2 * dtype_size(dtype)))
+    return fail(DO_ERR_INVALID_ARG, "p is NULL or not aligned to two elements");
+  if (bits == nullptr || !aligned(bits, 8)) return fail(DO_ERR_INVALID_ARG, "bits is NULL or not 8-byte aligned");
+  if (D == nullptr || !aligned(D, 4)) return fail(DO_ERR_INVALID_ARG, "D is NULL or not 4-byte aligned");
+  if (loss == nullptr || !aligned(loss, 8)) return fail(DO_ERR_INVALID_ARG, "loss is NULL or not 8-byte aligned");
+  if (grad != nullptr && !aligned(grad, 8)) return fail(DO_ERR_INVALID_ARG, "grad is not 8-byte aligned");
+  if (!(scale == scale) || scale - scale != 0.0) return fail(DO_ERR_INVALID_ARG, "scale must be finite");
+  dol::SurrogateArgs a{};
+  a.p = p;
+  a.bits = reinterpret_cast<const u64*>(bits);
+  a.D = D;
+  a.loss = loss;
+  a.grad = grad;
+  a.N = N;
+  a.W = (N + 63) / 64;
+  a.E = E;
+  a.L = L;
+  a.s64 = scale / ((double)N * (double)N * (double)k);
+  a.s32 = (float)a.s64;
+  DO_TRY(hip_status(dol::launch_fill_u64(reinterpret_cast<u64*>(loss), L, stream), "fill"));
+  return hip_status(profiled(stream, [&] { return dol::launch_surrogate(dtype, a, stream); }), "surrogate");
+}
+
 DOLOSS_API do_status do_stream_create(int32_t E, int32_t k, int64_t capacity_tokens, do_stream** out) {
   if (out == nullptr) return fail(DO_ERR_INVALID_ARG, "out is NULL");
   *out = nullptr;

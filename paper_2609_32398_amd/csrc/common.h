@@ -52,6 +52,20 @@ struct PathArgs {
   int64_t cacc_layer_elems;
 };
 
+// Arguments of the surrogate-loss kernel.
+struct SurrogateArgs {
+  const void* p;       // [L][N][E] routing probabilities (fp32 or bf16)
+  const u64* bits;     // [L][E][W] signatures
+  const uint32_t* D;   // [L][E][E] distances G
+  double* loss;        // [L], accumulated into (zeroed by the caller)
+  float* grad;         // nullable [L][N][E]
+  int64_t N, W;
+  int32_t E, L;
+  double s64;          // scale / (N^2 k)
+  float s32;
+  int32_t pad_;
+};
+
 struct DevInfo {
   int device;
   int cu_count;
@@ -72,6 +86,9 @@ hipError_t launch_gram_bits(const u64* bits, int64_t W, int32_t E, int32_t L, ui
 // cacc may alias D.
 hipError_t launch_finalize(const uint32_t* cacc, uint32_t* D, do_loss_result* out, int32_t E, int32_t L,
                            hipStream_t s);
+
+// Surrogate loss (Eq. 7) and its gradient; a.loss must be zero.
+hipError_t launch_surrogate(do_dtype dt, const SurrogateArgs& a, hipStream_t s);
 
 // Loss of arbitrary distance matrices.
 hipError_t launch_loss(const uint32_t* D, int32_t E, int32_t L, do_loss_result* out, hipStream_t s);

@@ -30,7 +30,7 @@ def _declared():
 def test_header_declares_the_path(dl):
     names = _declared()
     for must in ("do_topk_signature", "do_pairwise_hamming", "do_loss", "do_fused", "do_stream_create",
-                 "do_stream_append", "do_stream_append_many", "do_stream_finalize"):
+                 "do_stream_append", "do_stream_append_many", "do_stream_finalize", "do_surrogate"):
         assert must in names
 
 
@@ -96,6 +96,23 @@ def test_hamming_and_loss_reject(dl):
     assert _st(dl, "do_loss", None, 8, 1, FAKE, None) == 1
     assert _st(dl, "do_loss", FAKE, 8, 1, None, None) == 1
     assert _st(dl, "do_loss", FAKE, 0, 1, FAKE, None) == 1
+
+
+@pytest.mark.parametrize("args,expect", [
+    ((FAKE, 5, 64, 8, 2, 1, FAKE, FAKE, 1.0, FAKE, FAKE, None), 2),      # bad dtype
+    ((FAKE, 0, 64, 300, 2, 1, FAKE, FAKE, 1.0, FAKE, FAKE, None), 1),    # E > 256
+    ((FAKE, 0, 64, 8, 9, 1, FAKE, FAKE, 1.0, FAKE, FAKE, None), 1),      # k > E
+    ((FAKE + 4, 0, 64, 8, 2, 1, FAKE, FAKE, 1.0, FAKE, FAKE, None), 1),  # fp32 p not 8-byte aligned
+    ((FAKE, 0, 64, 8, 2, 1, None, FAKE, 1.0, FAKE, FAKE, None), 1),      # NULL bits
+    ((FAKE, 0, 64, 8, 2, 1, FAKE, None, 1.0, FAKE, FAKE, None), 1),      # NULL D
+    ((FAKE, 0, 64, 8, 2, 1, FAKE, FAKE, 1.0, None, FAKE, None), 1),      # NULL loss
+    ((FAKE, 0, 64, 8, 2, 1, FAKE, FAKE, 1.0, FAKE, FAKE + 4, None), 1),  # grad not 8-byte aligned
+    ((FAKE, 0, 64, 8, 2, 1, FAKE, FAKE, float("nan"), FAKE, FAKE, None), 1),  # scale not finite
+    ((FAKE, 0, 1 << 29, 8, 2, 1, FAKE, FAKE, 1.0, FAKE, FAKE, None), 4),  # (E-1) N >= 2^31
+])
+def test_surrogate_rejects(dl, args, expect):
+    assert _st(dl, "do_surrogate", *args) == expect
+    assert dl.lib().do_last_error()
 
 
 def test_stream_rejects_without_touching_the_device(dl):

@@ -7,6 +7,8 @@ Workload 4 (8 x 4,194,304 tokens x 256 experts) is compared in full on its
 first and last layer; on every layer, sampled token positions are compared
 with the oracle's Top-K of those tokens and the properties that hold at any
 size are checked (Eq. 2 zero-sum, row sums, symmetry, exact loss of D).
+The surrogate loss (Eq. 7) runs on the same tokens: sampled gradients against
+the oracle and the loss against its linearity in p.
 """
 import numpy as np
 import pytest
@@ -72,6 +74,34 @@ def test_workload3_stream_full(dl, orc, syn):
         s.close()
 
 
+def _surrogate_full(dl, orc, syn, scores, bits, D, k):
+    """Eq. 7 on the full workload (its scores are per-token probabilities):
+    the gradient of sampled tokens against the oracle, and the loss against
+    sum_t sum_i p_it dloss/dp_it (the loss is linear in p)."""
+    L, N, E = scores.shape
+    print(f"[case] surrogate on the full workload L={L} N={N} E={E}", flush=True)
+    loss, grad = dl.do_surrogate(scores, k, bits, D)
+    torch.cuda.synchronize()
+    lin = [(scores[l].double() * grad[l].double()).sum().item() for l in range(L)]
+    loss = loss.cpu().numpy()
+    for l in range(L):
+        assert loss[l] == pytest.approx(lin[l], rel=1e-6), (l, loss[l], lin[l])
+    rng = np.random.default_rng(44)
+    Dh = D.cpu().numpy().view(np.uint32)
+    for l in (0, L - 1):
+        words = bits_np(bits[l])
+        tok = np.sort(rng.choice(N, 512, replace=False))
+        p = scores[l][torch.from_numpy(tok).cuda()].cpu().numpy()
+        F = bits_at(words, tok)
+        # the oracle's 1/(n^2 k) for n sampled tokens, rescaled to the full N
+        _, ref = orc.surrogate(p, F, Dh[l], k, scale=(len(tok) / N) ** 2)
+        got = grad[l][torch.from_numpy(tok).cuda()].cpu().numpy().astype(np.float64)
+        tol = 1e-5 * np.abs(ref) + 1e-6 * np.abs(ref).max()
+        assert (np.abs(got - ref) <= tol).all(), f"layer {l}: sampled gradients differ"
+    del grad
+    torch.cuda.empty_cache()
+
+
 def test_workload4_full(dl, orc, syn):
     w = syn.WORKLOADS[4]
     L, N, E, k = w["layers"], w["n"], w["E"], w["k"]
@@ -80,6 +110,7 @@ def test_workload4_full(dl, orc, syn):
     scores, kept = upload_workload(syn, 4, L, keep=full)
     bits, D, out = dl.do_fused(scores, k, want_bits=True)
     torch.cuda.synchronize()
+    _surrogate_full(dl, orc, syn, scores, bits, D, k)
     del scores
     torch.cuda.empty_cache()
     recs = dl.loss_records(out)

@@ -1,0 +1,105 @@
+"""Surrogate DO-loss (Sec. 3.1.3, Eq. 7) on the GPU against the oracle.
+
+The signatures and distances given to do_surrogate come from the oracle, so
+these tests do not depend on the Top-K kernel.  Bar: the gradient within
+1e-5 relative of the fp64 oracle element by element (with an absolute floor
+of 1e-6 of the largest magnitude, for entries that cancel to ~0), the loss
+within 1e-5 relative.
+"""
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dl():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_32398_amd as p
+
+    p.lib()
+    return p
+
+
+def _softmax(x):
+    z = np.exp(x.astype(np.float64) - x.max(axis=1, keepdims=True))
+    return z / z.sum(axis=1, keepdims=True)
+
+
+def _probs(x, dtype):
+    p = _softmax(x).astype(np.float32)
+    if dtype == 1:  # bf16 bit patterns (round to nearest even)
+        u = p.view(np.uint32).astype(np.uint64)
+        u = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+        return u
+    return p
+
+
+def _grad_close(got, ref):
+    tol = 1e-5 * np.abs(ref) + 1e-6 * max(1e-300, np.abs(ref).max())
+    bad = np.abs(got.astype(np.float64) - ref) > tol
+    assert not bad.any(), f"{bad.sum()} gradient entries off, first {np.argwhere(bad)[:4].tolist()}"
+
+
+def _case(dl, orc, syn, seed, L, N, E, k, dtype, scale=1.0):
+    xs = [syn.normal(seed + l, N, E, 0) for l in range(L)]
+    ps = [_probs(x, dtype) for x in xs]
+    Fs = [orc.topk_signature(x, k) for x in xs]
+    bits = np.stack([orc.pack(F) for F in Fs])
+    Ds = np.stack([orc.hamming(F) for F in Fs])
+    p_dev = to_dev(np.concatenate(ps).reshape(L * N, E)).view(L, N, E)
+    b_dev = torch.from_numpy(bits.view(np.int64)).cuda()
+    D_dev = torch.from_numpy(Ds.view(np.int32)).cuda()
+    print(f"[case] surrogate L={L} N={N} E={E} k={k} dtype={dtype} scale={scale}", flush=True)
+    loss, grad = dl.do_surrogate(p_dev, k, b_dev, D_dev, scale=scale)
+    torch.cuda.synchronize()
+    loss = loss.cpu().numpy()
+    grad = grad.cpu().numpy()
+    for l in range(L):
+        ref_L, ref_g = orc.surrogate(ps[l], Fs[l], Ds[l], k, scale=scale)
+        assert loss[l] == pytest.approx(ref_L, rel=1e-5, abs=1e-12), (l, loss[l], ref_L)
+        _grad_close(grad[l], ref_g)
+    return loss, grad
+
+
+@pytest.mark.parametrize("N,E,k", [(64, 8, 2), (1000, 64, 6), (777, 100, 8), (513, 128, 8), (300, 200, 4),
+                                   (640, 256, 8), (130, 33, 3), (96, 256, 1)])
+@pytest.mark.parametrize("dtype", [0, 1])
+def test_surrogate_matches_oracle(dl, orc, syn, N, E, k, dtype):
+    _case(dl, orc, syn, 900 + E + k, 1, N, E, k, dtype)
+
+
+def test_surrogate_layers_and_scale(dl, orc, syn):
+    _case(dl, orc, syn, 950, 3, 700, 96, 4, 0, scale=0.125)
+
+
+def test_surrogate_without_gradient_output(dl, orc, syn):
+    N, E, k = 500, 64, 4
+    x = syn.normal(77, N, E, 0)
+    p = _probs(x, 0)
+    F = orc.topk_signature(x, k)
+    D = orc.hamming(F)
+    b = torch.from_numpy(orc.pack(F)[None].view(np.int64)).cuda()
+    Dd = torch.from_numpy(D[None].view(np.int32)).cuda()
+    loss, grad = dl.do_surrogate(to_dev(p)[None], k, b, Dd, want_grad=False)
+    torch.cuda.synchronize()
+    assert grad is None
+    assert loss.cpu().item() == pytest.approx(orc.surrogate(p, F, D, k, want_grad=False)[0], rel=1e-5)
+
+
+def test_surrogate_idle_expert_gradient_not_positive(dl, orc, syn):
+    N, E, k = 2000, 32, 2
+    x = syn.normal(81, N, E, 0)
+    x[:, 7] -= 100.0
+    F = orc.topk_signature(x, k)
+    D = orc.hamming(F)
+    p = _probs(x, 0)
+    b = torch.from_numpy(orc.pack(F)[None].view(np.int64)).cuda()
+    Dd = torch.from_numpy(D[None].view(np.int32)).cuda()
+    _, grad = dl.do_surrogate(to_dev(p)[None], k, b, Dd)
+    g = grad[0].cpu().numpy()
+    assert (g[:, 7] <= 0).all() and (g[:, 7] < 0).any()
