@@ -129,6 +129,9 @@ do_status do_fused(const void* scores, do_dtype dtype, int64_t N, int32_t E, int
  *   D     [L][E][E] device
  *   loss  [L] device doubles, overwritten
  *   grad  nullable, [L][N][E] device fp32 (8-byte aligned), overwritten
+ * Any set of bits is accepted as a signature; words in which some token has
+ * more than 8 set bits (not a top-k with k <= 8) take a slower path.  k only
+ * enters the normalisation.
  * Limits: E <= 256 and (E-1)*N < 2^31 (DO_ERR_OVERFLOW otherwise).  The loss
  * is accumulated in fp64 with atomic adds, so its last bits may differ
  * between runs; the gradient is deterministic.

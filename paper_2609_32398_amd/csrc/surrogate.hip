@@ -10,13 +10,14 @@
 // accumulated as sum_t sum_i p_it dL/dp_it in fp64.
 //
 // Work item: one signature word (64 tokens) of one layer and one range of up
-// to 128 experts i.  A block keeps the rows of G for its range in LDS,
-// transposed (gt[j][i], E x 128 u32, 128 KiB at 256 experts), with R for the
-// range and the signature words of the current tokens; lane l of a wave owns
-// experts 2l, 2l+1 of the range, so the loads of p and stores of the gradient
-// are coalesced rows and the reads of G for one selected expert j are a
-// contiguous LDS row.  The selected experts of a token come from its bit in
-// every expert's word (one ballot per 64 experts).
+// to 128 experts i, handled by one wave.  A block keeps the rows of G for its
+// range in LDS, transposed (gt[j][i], E x 128 u32, 128 KiB at 256 experts),
+// with R for the range; lane l owns experts 2l, 2l+1 of the range, so the
+// loads of p and the stores of the gradient are coalesced rows and the reads
+// of G for one selected expert j are a contiguous LDS row.  The selected
+// experts of a token are collected per item into a small LDS list (each
+// expert appends itself to the tokens set in its word), so a token's G rows
+// are read with eight independent LDS loads.
 #include <algorithm>
 
 #include "common.h"
@@ -24,10 +25,11 @@
 namespace dol {
 namespace {
 
-constexpr int kSurThreads = 512;
+constexpr int kSurThreads = 1024;
 constexpr int kSurWaves = kSurThreads / kWave;
-constexpr int kTokPerWave = kWave / kSurWaves;  // tokens of a 64-token word per wave
 constexpr int kRange = 128;  // experts per range (2 per lane)
+
+
 
 // Two consecutive probabilities as fp32 (one vector load when idx is even).
 template <typename T>
@@ -61,25 +63,170 @@ __device__ __forceinline__ double wave_sum(double v) {
   return v;
 }
 
+// Per-wave LDS scratch of one item: for each of its 64 tokens the number of
+// selected experts and the first kSurMaxK of their indices (unused entries
+// point at the all-zero row E of the tile).  A token with more selected
+// experts than that is summed from the signature words instead.
+constexpr int kSurMaxK = 8;
+struct WaveLists {
+  uint32_t cnt[64];
+  uint16_t idx[64][kSurMaxK];
+};
+
+// FULL: the range has 128 experts and E is even (every lane owns two valid,
+// pair-aligned experts), the common case; otherwise lanes and pairs are guarded.
+template <typename T, bool FULL>
+__device__ __forceinline__ void surrogate_item(const SurrogateArgs& a, const uint32_t* gt, WaveLists& wl, int E,
+                                               int ng, int iw, int r, int layer, int64_t w, int32_t R0, int32_t R1,
+                                               double& lacc, int lane) {
+  const int64_t W = a.W;
+  const u64* bl = a.bits + (int64_t)layer * E * W;
+  const int il0 = 2 * lane;
+  const bool v0 = FULL || il0 < iw, v1 = FULL || il0 + 1 < iw;
+  const bool even = FULL || (E & 1) == 0;
+  const int i0 = r * kRange + il0;
+  // words of experts g*64 + lane
+  u64 wg[4];
+#pragma unroll
+  for (int g = 0; g < 4; ++g) wg[g] = (g < ng && g * 64 + lane < E) ? bl[(int64_t)(g * 64 + lane) * W + w] : 0ull;
+  // token lists: expert g*64 + lane appends itself to the list of every token
+  // whose bit is set in its word (order within a list is irrelevant: summed)
+  wl.cnt[lane] = 0u;
+  {
+    const u64 z = 0x0001000100010001ull * (u64)E;  // the zero row E
+    *reinterpret_cast<u64*>(&wl.idx[lane][0]) = z;
+    *reinterpret_cast<u64*>(&wl.idx[lane][4]) = z;
+  }
+  __builtin_amdgcn_wave_barrier();
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    u64 bits = wg[g];
+    while (bits != 0ull) {
+      const int q = __builtin_ctzll(bits);
+      bits &= bits - 1;
+      const uint32_t slot = atomicAdd(&wl.cnt[q], 1u);
+      if (slot < (uint32_t)kSurMaxK) wl.idx[q][slot] = (uint16_t)(g * 64 + lane);
+    }
+  }
+  __builtin_amdgcn_wave_barrier();
+  // this lane's two experts: expert i0 (+1) sits in group 2r + lane/32 at lane i0 & 63
+  u64 w0, w1;
+  {
+    const u64 xa = r == 0 ? wg[0] : wg[2];
+    const u64 xb = r == 0 ? wg[1] : wg[3];
+    const u64 a0 = __shfl(xa, il0 & 63), b0 = __shfl(xb, il0 & 63);
+    const u64 a1 = __shfl(xa, (il0 + 1) & 63), b1 = __shfl(xb, (il0 + 1) & 63);
+    w0 = v0 ? (lane < 32 ? a0 : b0) : 0ull;
+    w1 = v1 ? (lane < 32 ? a1 : b1) : 0ull;
+  }
+  const int64_t tok0 = w * 64;
+  const int nt = (int)min((int64_t)64, a.N - tok0);
+  const int64_t row0 = (int64_t)layer * a.N + tok0;  // global row of token 0 of the word
+  const T* prow = reinterpret_cast<const T*>(a.p) + row0 * E;
+  float* grow = a.grad != nullptr ? a.grad + row0 * E : nullptr;
+  const uint32_t* gl = gt + il0;
+
+  // token tb: c = f R - sum_{j selected} G_ij for this lane's two experts
+  auto emit = [&](int tb, float pa, float pb, int32_t acc0, int32_t acc1) {
+    const int32_t c0 = (((w0 >> tb) & 1ull) ? R0 : 0) - acc0;
+    const int32_t c1 = (((w1 >> tb) & 1ull) ? R1 : 0) - acc1;
+    if (v0) {
+      lacc += (double)pa * (double)c0 + (double)pb * (double)c1;
+      if (grow != nullptr) {
+        float* g = grow + (int64_t)tb * E + i0;
+        if (FULL || (v1 && even)) {
+          *reinterpret_cast<float2*>(g) = float2{(float)c0 * a.s32, (float)c1 * a.s32};
+        } else {
+          g[0] = (float)c0 * a.s32;
+          if (v1) g[1] = (float)c1 * a.s32;
+        }
+      }
+    }
+  };
+  auto load_p = [&](int tb, float& pa, float& pb) {
+    pa = pb = 0.f;
+    if (tb < nt && v0) {
+      const int64_t off = (int64_t)tb * E + i0;
+      if (FULL || (v1 && even)) {
+        Prob<T>::pair(prow, off, pa, pb);
+      } else {
+        pa = Prob<T>::one(prow, off);
+        if (v1) pb = Prob<T>::one(prow, off + 1);
+      }
+    }
+  };
+
+  if (__ballot(wl.cnt[lane] > (uint32_t)kSurMaxK) == 0ull) {
+    for (int q0 = 0; q0 < nt; q0 += 16) {
+      // probabilities of 16 tokens, loaded together before this batch's stores
+      float xa[16], xb[16];
+#pragma unroll
+      for (int q = 0; q < 16; ++q) load_p(q0 + q, xa[q], xb[q]);
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        const int tb = q0 + q;
+        if (tb < nt) {  // wave-uniform
+          const uint4 lst = *reinterpret_cast<const uint4*>(&wl.idx[tb][0]);  // same address (and value) in every lane
+          const uint32_t lw[4] = {lst.x, lst.y, lst.z, lst.w};
+          uint2 gv[kSurMaxK];
+#pragma unroll
+          for (int rr = 0; rr < kSurMaxK; ++rr) {
+            const uint32_t j = (lw[rr >> 1] >> (16 * (rr & 1))) & 0xFFFFu;
+            gv[rr] = *reinterpret_cast<const uint2*>(gl + j * kRange);
+          }
+          int32_t acc0 = 0, acc1 = 0;
+#pragma unroll
+          for (int rr = 0; rr < kSurMaxK; ++rr) {
+            acc0 += (int32_t)gv[rr].x;
+            acc1 += (int32_t)gv[rr].y;
+          }
+          emit(tb, xa[q], xb[q], acc0, acc1);
+        }
+      }
+    }
+  } else {
+    // some token selected more experts than a list holds (signatures not made
+    // by a top-k with k <= kSurMaxK): sum over the set bits of every token
+    for (int tb = 0; tb < nt; ++tb) {
+      float pa, pb;
+      load_p(tb, pa, pb);
+      int32_t acc0 = 0, acc1 = 0;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {  // wg[g] is zero past the last group
+        u64 sel = __ballot((wg[g] >> tb) & 1ull);
+        while (sel != 0ull) {
+          const int j = g * 64 + __builtin_ctzll(sel);
+          sel &= sel - 1;
+          const uint2 v = *reinterpret_cast<const uint2*>(gl + j * kRange);
+          acc0 += (int32_t)v.x;
+          acc1 += (int32_t)v.y;
+        }
+      }
+      emit(tb, pa, pb, acc0, acc1);
+    }
+  }
+  __builtin_amdgcn_wave_barrier();  // the lists are rebuilt by the next item
+}
+
 template <typename T>
 __global__ __launch_bounds__(kSurThreads) void k_surrogate(const SurrogateArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int E = a.E;
   const int nr = (E + kRange - 1) / kRange;
-  uint32_t* gt = reinterpret_cast<uint32_t*>(smem);          // [E][kRange]: gt[j][il] = G[range + il][j]
-  int32_t* rr = reinterpret_cast<int32_t*>(gt + (size_t)E * kRange);  // [kRange] R_i for the range
-  u64* wd = reinterpret_cast<u64*>(rr + kRange);             // [E] signature words of the current tokens
+  uint32_t* gt = reinterpret_cast<uint32_t*>(smem);  // [E + 1][kRange]: gt[j][il] = G[range + il][j]; row E zero
+  int32_t* rr = reinterpret_cast<int32_t*>(gt + (size_t)(E + 1) * kRange);  // [kRange] R_i for the range
+  WaveLists* lists = reinterpret_cast<WaveLists*>(rr + kRange);              // [kSurWaves]
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const bool even = (E & 1) == 0;  // rows start on an even element: pairs are one vector access
+  const int ng = (E + 63) >> 6;  // 64-expert groups
   const int64_t W = a.W;
   const int64_t items = (int64_t)a.L * nr * W;
   const int64_t ib = (int64_t)blockIdx.x * items / gridDim.x;
   const int64_t ie = (int64_t)(blockIdx.x + 1) * items / gridDim.x;
   if (ib >= ie) return;
+  for (int il = tid; il < kRange; il += kSurThreads) gt[(size_t)E * kRange + il] = 0u;
 
-  int cur_lr = -1;  // layer * nr + range held in LDS
   double lacc = 0.0;
   int cur_layer = -1;
   auto flush_loss = [&]() {
@@ -88,96 +235,40 @@ __global__ __launch_bounds__(kSurThreads) void k_surrogate(const SurrogateArgs a
     lacc = 0.0;
   };
 
-  for (int64_t it = ib; it < ie; ++it) {
-    const int lr = (int)(it / W);
-    const int64_t w = it - (int64_t)lr * W;
+  // runs of items with one (layer, range): the tile is loaded once per run,
+  // then each wave takes every kSurWaves-th item of the run without barriers
+  for (int64_t sb = ib; sb < ie;) {
+    const int lr = (int)(sb / W);
+    const int64_t se = min(ie, (int64_t)(lr + 1) * W);
     const int layer = lr / nr, r = lr - layer * nr;
     const int iw = min(kRange, E - r * kRange);  // experts in this range
-    __syncthreads();  // previous item's readers of wd (and of the tile) are done
-    if (lr != cur_lr) {
-      if (layer != cur_layer) {
-        flush_loss();
-        cur_layer = layer;
-      }
-      const uint32_t* Dl = a.D + (int64_t)layer * E * E;
-      for (int idx = tid; idx < E * iw; idx += kSurThreads) {  // rows i of the range, read along j
-        const int il = idx / E, j = idx - il * E;
-        gt[j * kRange + il] = Dl[(int64_t)(r * kRange + il) * E + j];
-      }
-      __syncthreads();
-      for (int il = tid; il < iw; il += kSurThreads) {
-        int32_t acc = 0;
-        for (int j = 0; j < E; ++j) acc += (int32_t)gt[j * kRange + il];  // R_i = sum_j G_ij
-        rr[il] = acc;
-      }
-      cur_lr = lr;
+    if (layer != cur_layer) {
+      flush_loss();
+      cur_layer = layer;
     }
-    const u64* bl = a.bits + (int64_t)layer * E * W;
-    for (int e = tid; e < E; e += kSurThreads) wd[e] = bl[(int64_t)e * W + w];
+    __syncthreads();  // every wave is done with the previous tile
+    const uint32_t* Dl = a.D + (int64_t)layer * E * E;
+    for (int idx = tid; idx < E * kRange; idx += kSurThreads) {  // rows i of the range, read along j
+      const int il = idx / E, j = idx - il * E;
+      gt[j * kRange + il] = il < iw ? Dl[(int64_t)(r * kRange + il) * E + j] : 0u;
+    }
     __syncthreads();
-
-    // this lane's experts of the range and their words
-    const int il0 = 2 * lane, il1 = il0 + 1;
-    const bool v0 = il0 < iw, v1 = il1 < iw;
-    const int i0 = r * kRange + il0;
-    const u64 w0 = v0 ? wd[i0] : 0ull, w1 = v1 ? wd[i0 + 1] : 0ull;
-    const int32_t R0 = v0 ? rr[il0] : 0, R1 = v1 ? rr[il1] : 0;
-    // the words of experts lane, lane+64, ... (for the selection ballots)
-    u64 wg[4];
-#pragma unroll
-    for (int g = 0; g < 4; ++g) wg[g] = (g * 64 + lane < E) ? wd[g * 64 + lane] : 0ull;
-
-    const int64_t tok0 = w * 64;
-    const int64_t prow = (int64_t)layer * a.N;  // token row offset of this layer
-    // this wave's tokens of the word: prefetch their p values first
-    float pa[kTokPerWave], pb[kTokPerWave];
-#pragma unroll
-    for (int q = 0; q < kTokPerWave; ++q) {
-      const int64_t t = tok0 + wave * kTokPerWave + q;
-      pa[q] = pb[q] = 0.f;
-      if (t < a.N && v0) {
-        const int64_t base = (prow + t) * E + i0;
-        if (v1 && even)
-          Prob<T>::pair(a.p, base, pa[q], pb[q]);
-        else {
-          pa[q] = Prob<T>::one(a.p, base);
-          if (v1) pb[q] = Prob<T>::one(a.p, base + 1);
-        }
-      }
+    for (int il = tid; il < iw; il += kSurThreads) {
+      int32_t acc = 0;
+      for (int j = 0; j < E; ++j) acc += (int32_t)gt[j * kRange + il];  // R_i = sum_j G_ij
+      rr[il] = acc;
     }
-#pragma unroll
-    for (int q = 0; q < kTokPerWave; ++q) {
-      const int tb = wave * kTokPerWave + q;  // bit of the token in the words
-      const int64_t t = tok0 + tb;
-      if (t >= a.N) break;  // wave-uniform
-      int32_t acc0 = 0, acc1 = 0;
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        if (g * 64 >= E) break;
-        u64 m = __ballot(((wg[g] >> tb) & 1ull) != 0ull);
-        while (m != 0ull) {
-          const int j = g * 64 + __builtin_ctzll(m);
-          m &= m - 1;
-          const uint2 gv = *reinterpret_cast<const uint2*>(gt + j * kRange + il0);
-          acc0 += (int32_t)gv.x;
-          acc1 += (int32_t)gv.y;
-        }
-      }
-      const int32_t c0 = (((w0 >> tb) & 1ull) ? R0 : 0) - acc0;
-      const int32_t c1 = (((w1 >> tb) & 1ull) ? R1 : 0) - acc1;
-      if (v0) {
-        lacc += (double)pa[q] * (double)c0 + (double)pb[q] * (double)c1;
-        if (a.grad != nullptr) {
-          float* g = a.grad + (prow + t) * E + i0;
-          if (v1 && even) {
-            *reinterpret_cast<float2*>(g) = float2{(float)c0 * a.s32, (float)c1 * a.s32};
-          } else {
-            g[0] = (float)c0 * a.s32;
-            if (v1) g[1] = (float)c1 * a.s32;
-          }
-        }
-      }
+    __syncthreads();
+    const int32_t R0 = 2 * lane < iw ? rr[2 * lane] : 0, R1 = 2 * lane + 1 < iw ? rr[2 * lane + 1] : 0;
+    const bool full = iw == kRange && (E & 1) == 0;
+    for (int64_t it = sb + wave; it < se; it += kSurWaves) {
+      const int64_t w = it - (int64_t)lr * W;
+      if (full)
+        surrogate_item<T, true>(a, gt, lists[wave], E, ng, iw, r, layer, w, R0, R1, lacc, lane);
+      else
+        surrogate_item<T, false>(a, gt, lists[wave], E, ng, iw, r, layer, w, R0, R1, lacc, lane);
     }
+    sb = se;
   }
   flush_loss();
 }
@@ -186,7 +277,7 @@ __global__ __launch_bounds__(kSurThreads) void k_surrogate(const SurrogateArgs a
 
 hipError_t launch_surrogate(do_dtype dt, const SurrogateArgs& a, hipStream_t s) {
   const int nr = (a.E + kRange - 1) / kRange;
-  const size_t lds = (size_t)a.E * kRange * 4 + kRange * 4 + (size_t)a.E * 8;
+  const size_t lds = (size_t)(a.E + 1) * kRange * 4 + kRange * 4 + kSurWaves * sizeof(WaveLists);
   const void* kern = dt == DO_F32 ? reinterpret_cast<const void*>(k_surrogate<float>)
                                   : reinterpret_cast<const void*>(k_surrogate<uint16_t>);
   hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);

@@ -103,3 +103,28 @@ def test_surrogate_idle_expert_gradient_not_positive(dl, orc, syn):
     _, grad = dl.do_surrogate(to_dev(p)[None], k, b, Dd)
     g = grad[0].cpu().numpy()
     assert (g[:, 7] <= 0).all() and (g[:, 7] < 0).any()
+
+
+@pytest.mark.parametrize("N,E", [(200, 40), (130, 256)])
+def test_surrogate_general_signatures(dl, orc, syn, N, E):
+    # signatures that are not a top-k: per token anywhere from 0 to E selected
+    # experts, so some words hold tokens with more selections than the
+    # kernel's per-token list keeps and take its general path
+    rng = np.random.default_rng(E)
+    dens = rng.uniform(0.0, 1.0, size=N)
+    dens[::5] = 0.02
+    F = (rng.uniform(size=(E, N)) < dens[None, :]).astype(np.uint8)
+    F[:, 3] = 0
+    F[:, 4] = 1
+    k = 8
+    x = syn.normal(97, N, E, 0)
+    p = _probs(x, 0)
+    D = orc.hamming(F)
+    b = torch.from_numpy(orc.pack(F)[None].view(np.int64)).cuda()
+    Dd = torch.from_numpy(D[None].view(np.int32)).cuda()
+    print(f"[case] surrogate general signatures N={N} E={E}", flush=True)
+    loss, grad = dl.do_surrogate(to_dev(p)[None], k, b, Dd)
+    torch.cuda.synchronize()
+    ref_L, ref_g = orc.surrogate(p, F, D, k)
+    assert loss.cpu().item() == pytest.approx(ref_L, rel=1e-5, abs=1e-12)
+    _grad_close(grad[0].cpu().numpy(), ref_g)
