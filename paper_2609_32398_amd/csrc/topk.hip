@@ -66,6 +66,13 @@ __device__ __forceinline__ int bt_swz(int s) { return (s & 7) << 2; }
 // the read-once stream ages out of L2 before the partially written signature
 // lines, which then merge there into whole lines before eviction.
 constexpr int kStreamPolicy = 2;
+// Units of signature stores held in registers (see batch_flush), and the
+// (expert, word pair) items a lane holds per unit: 4 * E/8 items per wave.
+template <int EPW>
+struct StoreBatch {
+  static constexpr int kUnits = EPW > 128 ? 4 : 2;
+  static constexpr int kItems = EPW > 128 ? 2 : 1;
+};
 
 // s_waitcnt vmcnt(0) (expcnt and lgkmcnt left at their maxima)
 #define DOL_WAIT_VMEM() __builtin_amdgcn_s_waitcnt(0x0F70)
@@ -637,12 +644,61 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
   };
   Pending pend{};
   bool have_pend = false;
+  typedef StoreBatch<EPW> SB;
+  v2u64 sreg[SB::kUnits][SB::kItems];  // batched signature stores (see batch_flush)
+  u64* sb_lb = nullptr;
+  int64_t sb_w0 = 0;
+  int sb_n = 0;
   // This wave's share of the pending unit's signature stores: experts
   // [wave*E/8, (wave+1)*E/8), 64 bytes (8 words) per expert as four 16-byte
   // stores when the unit starts on an even word, else word by word.
-  auto store_share = [&](const u64* pbt) {
+  // The stores of plain units (8 words, even first word, no word shared with
+  // a neighbouring segment) are held in registers for up to SB::kUnits
+  // consecutive units of one layer and issued together, so each expert row
+  // receives 64 * SB::kUnits contiguous bytes at once (fewer read/write
+  // turnarounds in HBM than one 64-byte piece per unit).  Only for E <= 256.
+  auto batch_flush = [&]() __attribute__((always_inline)) {
+    if (sb_n == 0) return;
+    const int e_lo = (wave * E) >> 3, e_hi = ((wave + 1) * E) >> 3;
+#pragma unroll
+    for (int i = 0; i < SB::kItems; ++i) {
+      const int item = e_lo * 4 + lane + i * kWave;
+      if (item < e_hi * 4) {
+        u64* dst = sb_lb + (int64_t)(item >> 2) * a.W + sb_w0 + (item & 3) * 2;
+#pragma unroll
+        for (int j = 0; j < SB::kUnits; ++j)
+          if (j < sb_n) *reinterpret_cast<v2u64*>(dst + 8 * j) = sreg[j][i];
+      }
+    }
+    sb_n = 0;
+  };
+  auto store_share = [&](const u64* pbt) __attribute__((always_inline)) {
     if (pend.lb == nullptr) return;
     const int e_lo = (wave * E) >> 3, e_hi = ((wave + 1) * E) >> 3;
+    if (EPW <= 256 && (pend.w0 & 1) == 0 && pend.cnt == kFusedWaves && !pend.shared_lo && pend.shared_hi < 0) {
+      if (sb_n > 0 && (sb_lb != pend.lb || sb_w0 + 8 * sb_n != pend.w0)) batch_flush();
+      if (sb_n == 0) {
+        sb_lb = pend.lb;
+        sb_w0 = pend.w0;
+      }
+      v2u64 v[SB::kItems];
+#pragma unroll
+      for (int i = 0; i < SB::kItems; ++i) {
+        const int item = e_lo * 4 + lane + i * kWave;
+        const int e = item >> 2, s0 = (item & 3) * 2;
+        v[i] = item < e_hi * 4 ? v2u64{pbt[s0 * EPW + (e ^ bt_swz(s0))], pbt[(s0 + 1) * EPW + (e ^ bt_swz(s0 + 1))]}
+                               : v2u64{0ull, 0ull};
+      }
+#pragma unroll
+      for (int j = 0; j < SB::kUnits; ++j)
+        if (j == sb_n) {
+#pragma unroll
+          for (int i = 0; i < SB::kItems; ++i) sreg[j][i] = v[i];
+        }
+      if (++sb_n == SB::kUnits) batch_flush();
+      return;
+    }
+    batch_flush();
     auto plain = [&](int s_) { return !((s_ == 0 && pend.shared_lo) || s_ == pend.shared_hi); };
     auto put = [&](int e_, int s_, u64 word) {
       u64* dst = pend.lb + (int64_t)e_ * a.W + pend.w0 + s_;
@@ -840,6 +896,7 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
   }
   // the last unit
   store_share(bt_all + (buf ^ 1) * kFusedWaves * EPW);
+  batch_flush();
   gram_slots(bt_all + (buf ^ 1) * kFusedWaves * EPW, 0, kFusedWaves);
   flush(pend.layer);
 }
