@@ -508,18 +508,21 @@ typedef unsigned long long v2u64 __attribute__((ext_vector_type(2)));
 // ---------------------------------------------------------------------------
 // Top-K (+ Gram) kernel.  Work unit: 8 consecutive signature words (512
 // output positions) of one segment, starting 8-aligned within it; one unit
-// per block step, one word (64 tokens) per wave.  One persistent block per CU
-// slot takes the contiguous unit range [b*U/G, (b+1)*U/G).
+// per block step, one word (64 tokens) per wave.  The grid is persistent
+// (one block per CU slot); each block walks the units of its schedule: either
+// one contiguous range, or interleaved groups of consecutive units (see
+// next_unit and launch_one).
 //
 // Software pipeline: the signature stores and the Gram of a unit run during
 // the next unit (stores right after its first chunk arrives, one Gram slot
 // after each ranked chunk), so they overlap other waves' ranking instead of
 // following every barrier at once.  Gram accumulators are flushed when the
 // layer changes and at the end.  flags bit 0: fast path allowed (16-byte
-// rows, k <= 8, E <= 256).
+// rows, k <= 8, E <= 256); bit 1: XCD-adjacent group placement.  gu: units
+// per schedule group.
 // ---------------------------------------------------------------------------
 template <typename T, int EP, int GM>
-__global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, const PathArgs a, int flags) {
+__global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, const PathArgs a, int flags, int64_t gu) {
   (void)tab_arg;  // read through `tab` below (it is the first kernel argument)
   const SegTablePtr tab = (SegTablePtr)__builtin_amdgcn_kernarg_segment_ptr();
   constexpr int EPW = EP < 32 ? 32 : EP;  // signature words per slot of the bit tile
@@ -537,10 +540,24 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
   const int nch = (rowv + 7) >> 3;
   unsigned char* st = smem + wave * 2 * kChunkBytes;  // this wave's two stage buffers
 
+  // Unit schedule: groups of `gu` consecutive units; block b takes groups
+  // pos(b), pos(b) + G, pos(b) + 2G, ... (G = grid size), so at any time the
+  // blocks work on one contiguous stretch of units and their signature stores
+  // land side by side in every expert row.  With `xcd` set, pos(b) puts the
+  // blocks that share an XCD (round-robin dispatch: b mod 8) on adjacent groups.
   const int64_t U = tab->tile_start[tab->nseg];
-  const int64_t ug = (int64_t)blockIdx.x * U / gridDim.x;
-  const int64_t ue = (int64_t)(blockIdx.x + 1) * U / gridDim.x;
-  if (ug >= ue) return;
+  const int G = gridDim.x;
+  const int b = blockIdx.x;
+  const int pos = (flags & 2) && (G & 7) == 0 ? (b & 7) * (G >> 3) + (b >> 3) : b;
+  const int64_t ug = (int64_t)pos * gu;
+  if (ug >= U) return;
+  // unit after u in this block's schedule (U when there is none)
+  auto next_unit = [&](int64_t u_) -> int64_t {
+    const int64_t v = u_ + 1;
+    if (v % gu != 0) return v < U ? v : U;
+    const int64_t w = v + (int64_t)(G - 1) * gu;
+    return w < U ? w : U;
+  };
 
   PopcGram<EPW, kFusedThreads, GM == kGramPopc> pg;
   if (GM == kGramPopc) pg.init(tid, E);
@@ -761,19 +778,21 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
   if (fast && tl0 + wave < sv.words) dma(sv, t0w, 0, st);
 
   int buf = 0;
-  for (int64_t u = ug; u < ue; buf ^= 1) {
+  for (int64_t u = ug; u < U; buf ^= 1) {
     const int cnt = (int)min((int64_t)kFusedWaves, sv.words - tl0);  // words in this unit
     // next unit and its segment (wave-uniform)
-    const int64_t un = u + 1;
+    const int64_t un = next_unit(u);
     int seg_n = seg;
     Seg svn = sv;
     int64_t tl0n = tl0 + 8;
-    if (un < ue && un >= tab->tile_start[seg + 1]) {
-      seg_n = seg_of(tab, un, seg);
-      svn = load_seg(tab, seg_n);
+    if (un < U) {
+      if (un >= tab->tile_start[seg + 1]) {
+        seg_n = seg_of(tab, un, seg);
+        svn = load_seg(tab, seg_n);
+      }
       tl0n = 8 * (un - svn.u_begin);
     }
-    const bool next_mine = un < ue && tl0n + wave < svn.words;
+    const bool next_mine = un < U && tl0n + wave < svn.words;
     const int64_t t0n = (svn.w_first + tl0n + wave) * 64 - svn.off;
 
     u64* bt = bt_all + buf * kFusedWaves * EPW;
@@ -911,6 +930,29 @@ int gram_mode() {
   return g_gram_mode;
 }
 
+// Unit schedule of the Top-K kernel.  gu < 0: chosen per launch (below);
+// DOLOSS_SCHED overrides it for tuning: "c" = one contiguous range per
+// block, "i<n>" = interleaved groups of n units, "x<n>" = the same with
+// XCD-adjacent placement.
+struct Sched {
+  int64_t gu;
+  bool xcd;
+};
+bool g_sched_read = false;
+Sched g_sched{-1, false};
+Sched schedule() {
+  if (!g_sched_read) {
+    const char* v = getenv("DOLOSS_SCHED");
+    if (v != nullptr && v[0] == 'c') g_sched = Sched{0, false};
+    if (v != nullptr && (v[0] == 'i' || v[0] == 'x')) {
+      const int n = atoi(v + 1);
+      g_sched = Sched{n > 0 ? n : 4, v[0] == 'x'};
+    }
+    g_sched_read = true;
+  }
+  return g_sched;
+}
+
 template <typename T, int EP, int GM>
 hipError_t launch_one(const SegTable& tab, const PathArgs& a, bool fast, hipStream_t s) {
   constexpr int EPW = EP < 32 ? 32 : EP;
@@ -925,7 +967,22 @@ hipError_t launch_one(const SegTable& tab, const PathArgs& a, bool fast, hipStre
   const int64_t units = tab.tile_start[tab.nseg];
   int64_t blocks = std::min<int64_t>((int64_t)di.cu_count * occ, units);
   blocks = std::max<int64_t>(blocks, 1);
-  hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kFusedThreads), lds, s, tab, a, fast ? 1 : 0);
+  // Interleaved groups of 4 units with XCD-adjacent placement keep the
+  // signature stores of all blocks side by side; a block then changes output
+  // layer at every group, so that schedule is used only when every layer
+  // spans several rounds of groups (or the launch has one output layer).
+  Sched sc = schedule();
+  if (sc.gu < 0) {
+    int nl = 1;
+    for (int i = 1; i < tab.nseg; ++i) nl += tab.s[i].layer != tab.s[i - 1].layer;
+    const bool inter = nl == 1 || units / nl >= 4 * 4 * blocks;
+    sc.gu = inter ? 4 : 0;
+    sc.xcd = inter;
+  }
+  int64_t gu = sc.gu;
+  if (gu <= 0 || gu * blocks > units) gu = (units + blocks - 1) / blocks;  // contiguous ranges
+  const int flags = (fast ? 1 : 0) | (sc.xcd ? 2 : 0);
+  hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kFusedThreads), lds, s, tab, a, flags, gu);
   return hipGetLastError();
 }
 
