@@ -44,7 +44,9 @@ namespace {
 
 typedef uint32_t v4u __attribute__((ext_vector_type(4)));
 typedef int v4i __attribute__((ext_vector_type(4)));
-typedef int v16i __attribute__((ext_vector_type(16)));
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+typedef float v16f __attribute__((ext_vector_type(16)));
 typedef short v2s __attribute__((ext_vector_type(2)));
 
 // Per wave, two 8 KiB stage buffers of 64 rows x 128 bytes.  Piece q of row r
@@ -367,44 +369,55 @@ __device__ __forceinline__ WaveTiles wave_tiles(int T, int w) {
   return t;
 }
 
-// 16 signature bits -> 16 bytes of 0/1 (byte b = bit b).
-__device__ __forceinline__ v4i expand16(uint32_t b) {
-  v4i r;
-  r.x = (int)((((b >> 0) & 0xFu) * 0x00204081u) & 0x01010101u);
-  r.y = (int)((((b >> 4) & 0xFu) * 0x00204081u) & 0x01010101u);
-  r.z = (int)((((b >> 8) & 0xFu) * 0x00204081u) & 0x01010101u);
-  r.w = (int)((((b >> 12) & 0xFu) * 0x00204081u) & 0x01010101u);
+// 32 signature bits -> 32 fp4 (e2m1) operands of an MFMA: register d holds
+// bits d, d+4, ..., d+28 as nibbles 0..7, each 0b0001 (0.5) or 0b0000 (0.0).
+// Every bit lands in exactly one nibble; the token order along k does not
+// matter because the A and B fragments of a Gram come from the same mapping.
+__device__ __forceinline__ v8i expand32_fp4(uint32_t b) {
+  v8i r;
+  r[0] = (int)(b & 0x11111111u);
+  r[1] = (int)((b >> 1) & 0x11111111u);
+  r[2] = (int)((b >> 2) & 0x11111111u);
+  r[3] = (int)((b >> 3) & 0x11111111u);
+  r[4] = r[5] = r[6] = r[7] = 0;  // fp4 operands use the low four registers
   return r;
 }
 
-// MFMA shapes for TS-expert tiles.  A and B operands of lane l hold the same
-// k indices, so one expanded fragment serves as both operands of a Gram.
-//   TS = 32: v_mfma_i32_32x32x32_i8, lane l = expert l%32, k-step ks covers
-//            tokens 32*ks + 16*(l/32) .. +15 of the word; C row 8*(r/4)+4*(l/32)+r%4, col l%32
-//   TS = 16: v_mfma_i32_16x16x64_i8, lane l = expert l%16, tokens 16*(l/16) .. +15;
+// MFMA shapes for TS-expert tiles, fp4 operands with block scale 2^1 on both
+// sides, so that every co-occurring token adds 0.5 * 2 * 0.5 * 2 = 1.0 to the
+// fp32 accumulator (exact while a count stays below 2^24).  A and B operands
+// of lane l hold the same k indices, so one expanded fragment serves as both
+// operands of a Gram.
+//   TS = 32: v_mfma_scale_f32_32x32x64_f8f6f4, one signature word per
+//            instruction; lane l = expert l%32, bits 32*(l/32) .. +31 of the word;
+//            C row 8*(r/4)+4*(l/32)+r%4, col l%32
+//   TS = 16: v_mfma_scale_f32_16x16x128_f8f6f4, two words per instruction;
+//            lane l = expert l%16, 32-bit quarter l/16 of the word pair;
 //            C row 4*(l/16)+r, col l%16
+constexpr int kFp4 = 4;        // cbsz / blgp operand format code of e2m1
+constexpr int kScaleTwo = 128; // E8M0 block scale 2^(128-127)
 template <int TS>
 struct Mfma;
 template <>
 struct Mfma<32> {
-  typedef v16i Acc;
-  static constexpr int kSteps = 2, kRegs = 16;
+  typedef v16f Acc;
+  static constexpr int kWords = 1, kRegs = 16;
   __device__ static __forceinline__ int expert(int tile, int lane) { return tile * 32 + (lane & 31); }
-  __device__ static __forceinline__ int chunk16(int ks, int lane) { return ks * 2 + (lane >> 5); }
-  __device__ static __forceinline__ Acc mac(v4i a, v4i b, Acc c) {
-    return __builtin_amdgcn_mfma_i32_32x32x32_i8(a, b, c, 0, 0, 0);
+  __device__ static __forceinline__ int quarter(int lane) { return lane >> 5; }
+  __device__ static __forceinline__ Acc mac(v8i a, v8i b, Acc c) {
+    return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, kFp4, kFp4, 0, kScaleTwo, 0, kScaleTwo);
   }
   __device__ static __forceinline__ int row(int r, int lane) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
   __device__ static __forceinline__ int col(int lane) { return lane & 31; }
 };
 template <>
 struct Mfma<16> {
-  typedef v4i Acc;
-  static constexpr int kSteps = 1, kRegs = 4;
+  typedef v4f Acc;
+  static constexpr int kWords = 2, kRegs = 4;
   __device__ static __forceinline__ int expert(int tile, int lane) { return tile * 16 + (lane & 15); }
-  __device__ static __forceinline__ int chunk16(int, int lane) { return lane >> 4; }
-  __device__ static __forceinline__ Acc mac(v4i a, v4i b, Acc c) {
-    return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
+  __device__ static __forceinline__ int quarter(int lane) { return lane >> 4; }
+  __device__ static __forceinline__ Acc mac(v8i a, v8i b, Acc c) {
+    return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, kFp4, kFp4, 0, kScaleTwo, 0, kScaleTwo);
   }
   __device__ static __forceinline__ int row(int r, int lane) { return 4 * (lane >> 4) + r; }
   __device__ static __forceinline__ int col(int lane) { return lane & 15; }
@@ -418,26 +431,26 @@ struct GramShape {
   static constexpr int T = EPW / TS;
 };
 
-// Accumulate the wave's pair slots over slots [s0, s1) of the bit tile.
+// Accumulate the wave's pair slots over slots [s0, s1) of the bit tile; s0
+// and s1 are multiples of Mfma<TS>::kWords.
 template <int TS>
 __device__ __forceinline__ void mfma_slots(typename Mfma<TS>::Acc (&acc)[kGP], const WaveTiles& wt, const u64* bt,
                                            int stride, int s0, int s1, int lane) {
   if (wt.act == 0) return;
   const bool need[4] = {(wt.act & 0x1B) != 0, (wt.act & 0x6) != 0, (wt.act & 0xC) != 0, (wt.act & 0x10) != 0};
+  const int q = Mfma<TS>::quarter(lane);
 #pragma unroll 1
-  for (int s = s0; s < s1; ++s) {  // not unrolled: keeps the fragment registers to one word's worth
-    const uint16_t* w16 = reinterpret_cast<const uint16_t*>(bt + s * stride);
+  for (int s = s0; s < s1; s += Mfma<TS>::kWords) {  // not unrolled: keeps the fragment registers to one step's worth
+    const int ws = s + (q >> 1);                      // the word this lane reads
+    const uint32_t* w32 = reinterpret_cast<const uint32_t*>(bt + ws * stride);
+    v8i f[4];
 #pragma unroll
-    for (int ks = 0; ks < Mfma<TS>::kSteps; ++ks) {
-      v4i f[4];
+    for (int l = 0; l < 4; ++l)
+      f[l] = need[l] ? expand32_fp4(w32[(Mfma<TS>::expert(wt.tile[l], lane) ^ bt_swz(ws)) * 2 + (q & 1)])
+                     : v8i{0, 0, 0, 0, 0, 0, 0, 0};
 #pragma unroll
-      for (int l = 0; l < 4; ++l)
-        f[l] = need[l] ? expand16(w16[(Mfma<TS>::expert(wt.tile[l], lane) ^ bt_swz(s)) * 4 + Mfma<TS>::chunk16(ks, lane)])
-                       : v4i{0, 0, 0, 0};
-#pragma unroll
-      for (int p = 0; p < kGP; ++p)
-        if (wt.act & (1 << p)) acc[p] = Mfma<TS>::mac(f[slot_a(p)], f[slot_b(p)], acc[p]);
-    }
+    for (int p = 0; p < kGP; ++p)
+      if (wt.act & (1 << p)) acc[p] = Mfma<TS>::mac(f[slot_a(p)], f[slot_b(p)], acc[p]);
   }
 }
 
@@ -458,7 +471,7 @@ __device__ __forceinline__ void mfma_flush(const typename Mfma<TS>::Acc (&acc)[k
     for (int r = 0; r < Mfma<TS>::kRegs; ++r) {
       const int gi = TS * I + Mfma<TS>::row(r, lane);
       const int gj = TS * J + Mfma<TS>::col(lane);
-      const uint32_t v = (uint32_t)acc[p][r];
+      const uint32_t v = (uint32_t)acc[p][r];  // an exact integer count
       // a diagonal tile pair holds every pair of its experts twice; keep one
       const bool keep = (I != J || gi <= gj) && gi < E && gj < E && v != 0u;
       if (keep) atomicAdd(&c[(int64_t)min(gi, gj) * E + max(gi, gj)], v);
@@ -540,23 +553,34 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
   const int nch = (rowv + 7) >> 3;
   unsigned char* st = smem + wave * 2 * kChunkBytes;  // this wave's two stage buffers
 
-  // Unit schedule: groups of `gu` consecutive units; block b takes groups
-  // pos(b), pos(b) + G, pos(b) + 2G, ... (G = grid size), so at any time the
-  // blocks work on one contiguous stretch of units and their signature stores
-  // land side by side in every expert row.  With `xcd` set, pos(b) puts the
-  // blocks that share an XCD (round-robin dispatch: b mod 8) on adjacent groups.
+  // Unit schedule: the unit range [lo, hi) of a block's partition is cut into
+  // groups of `gu` consecutive units, and the Gs blocks of the partition take
+  // groups pos, pos + Gs, pos + 2 Gs, ...  Contiguous ranges are the case of
+  // one group per block.  flags bits 1-2 select the partition and placement:
+  //   0: one partition [0, U), pos = b
+  //   1: one partition, blocks that share an XCD (round-robin dispatch:
+  //      b mod 8) on adjacent groups
+  //   2: eight partitions, one per XCD (b mod 8), of U/8 units each; the
+  //      XCD's blocks work on adjacent groups of its partition, so their
+  //      signature stores land side by side while each block stays in few
+  //      layers (few Gram flushes, and those of different XCDs go to
+  //      different layers)
   const int64_t U = tab->tile_start[tab->nseg];
   const int G = gridDim.x;
   const int b = blockIdx.x;
-  const int pos = (flags & 2) && (G & 7) == 0 ? (b & 7) * (G >> 3) + (b >> 3) : b;
-  const int64_t ug = (int64_t)pos * gu;
-  if (ug >= U) return;
+  const int smode = (G & 7) == 0 ? (flags >> 1) & 3 : 0;
+  const int64_t lo = smode == 2 ? (int64_t)(b & 7) * U / 8 : 0;
+  const int64_t hi = smode == 2 ? (int64_t)((b & 7) + 1) * U / 8 : U;
+  const int Gs = smode == 2 ? G >> 3 : G;
+  const int pos = smode == 2 ? b >> 3 : smode == 1 ? (b & 7) * (G >> 3) + (b >> 3) : b;
+  const int64_t ug = lo + (int64_t)pos * gu;
+  if (ug >= hi) return;
   // unit after u in this block's schedule (U when there is none)
   auto next_unit = [&](int64_t u_) -> int64_t {
     const int64_t v = u_ + 1;
-    if (v % gu != 0) return v < U ? v : U;
-    const int64_t w = v + (int64_t)(G - 1) * gu;
-    return w < U ? w : U;
+    if ((v - lo) % gu != 0) return v < hi ? v : U;
+    const int64_t w = v + (int64_t)(Gs - 1) * gu;
+    return w < hi ? w : U;
   };
 
   PopcGram<EPW, kFusedThreads, GM == kGramPopc> pg;
@@ -567,7 +591,7 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
 #pragma unroll
     for (int p = 0; p < kGP; ++p)
 #pragma unroll
-      for (int r = 0; r < Mfma<GS::TS>::kRegs; ++r) acc[p][r] = 0;
+      for (int r = 0; r < Mfma<GS::TS>::kRegs; ++r) acc[p][r] = 0.0f;
   };
   zero_acc();
 
@@ -649,6 +673,10 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
       }
     }
   };
+
+  constexpr int kGramStep = GM == kGramMfma ? Mfma<GS::TS>::kWords : 1;  // slots per Gram step
+  constexpr int kMaxAccUnits = ((1 << 24) / 512) - 1;  // units per flush at most (counts < 2^24)
+  int acc_units = 0;
 
   // The unit whose bit tile is complete and whose stores and Gram are pending.
   struct Pending {
@@ -840,7 +868,7 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
           else
             rank_chunk<T, false>(cur, lane, c * 8, vmask, top, rej);
           if (gram_done < kFusedWaves) {
-            const int s_end = ((c + 1) * kFusedWaves) / nch;
+            const int s_end = (((c + 1) * kFusedWaves) / nch) & ~(kGramStep - 1);
             gram_slots(pbt, gram_done, s_end);
             gram_done = s_end;
           }
@@ -899,7 +927,12 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
     if (!stored) store_share(pbt);
     if (gram_done < kFusedWaves) gram_slots(pbt, gram_done, kFusedWaves);
     __syncthreads();  // this unit's bit tile is complete; the pending unit's tile is free
-    if (have_pend && pend.layer != sv.layer) flush(pend.layer);
+    // the fp32 Gram accumulators hold exact counts below 2^24: flush at a
+    // layer change and before a block has accumulated 2^24 tokens
+    if (have_pend && (pend.layer != sv.layer || ++acc_units >= kMaxAccUnits)) {
+      flush(pend.layer);
+      acc_units = 0;
+    }
     pend.lb = a.bits != nullptr ? a.bits + (int64_t)sv.layer * a.bits_layer_words : nullptr;
     pend.w0 = sv.w_first + tl0;
     pend.cnt = cnt;
@@ -932,21 +965,21 @@ int gram_mode() {
 
 // Unit schedule of the Top-K kernel.  gu < 0: chosen per launch (below);
 // DOLOSS_SCHED overrides it for tuning: "c" = one contiguous range per
-// block, "i<n>" = interleaved groups of n units, "x<n>" = the same with
-// XCD-adjacent placement.
+// block, "i<n>" / "x<n>" / "p<n>" = groups of n units in placement mode 0 / 1
+// / 2 (see k_topk).
 struct Sched {
   int64_t gu;
-  bool xcd;
+  int mode;
 };
 bool g_sched_read = false;
-Sched g_sched{-1, false};
+Sched g_sched{-1, 0};
 Sched schedule() {
   if (!g_sched_read) {
     const char* v = getenv("DOLOSS_SCHED");
-    if (v != nullptr && v[0] == 'c') g_sched = Sched{0, false};
-    if (v != nullptr && (v[0] == 'i' || v[0] == 'x')) {
+    if (v != nullptr && v[0] == 'c') g_sched = Sched{0, 0};
+    if (v != nullptr && (v[0] == 'i' || v[0] == 'x' || v[0] == 'p')) {
       const int n = atoi(v + 1);
-      g_sched = Sched{n > 0 ? n : 4, v[0] == 'x'};
+      g_sched = Sched{n > 0 ? n : 4, v[0] == 'i' ? 0 : v[0] == 'x' ? 1 : 2};
     }
     g_sched_read = true;
   }
@@ -971,17 +1004,14 @@ hipError_t launch_one(const SegTable& tab, const PathArgs& a, bool fast, hipStre
   // signature stores of all blocks side by side; a block then changes output
   // layer at every group, so that schedule is used only when every layer
   // spans several rounds of groups (or the launch has one output layer).
+  // Default: eight XCD partitions, groups of 4 units (placement mode 2).
   Sched sc = schedule();
-  if (sc.gu < 0) {
-    int nl = 1;
-    for (int i = 1; i < tab.nseg; ++i) nl += tab.s[i].layer != tab.s[i - 1].layer;
-    const bool inter = nl == 1 || units / nl >= 4 * 4 * blocks;
-    sc.gu = inter ? 4 : 0;
-    sc.xcd = inter;
-  }
+  if (sc.gu < 0) sc = Sched{4, 2};
   int64_t gu = sc.gu;
-  if (gu <= 0 || gu * blocks > units) gu = (units + blocks - 1) / blocks;  // contiguous ranges
-  const int flags = (fast ? 1 : 0) | (sc.xcd ? 2 : 0);
+  const int64_t per_part = sc.mode == 2 ? (units + 7) / 8 : units;
+  const int64_t gs = sc.mode == 2 ? std::max<int64_t>(blocks / 8, 1) : blocks;
+  if (gu <= 0 || gu * gs > per_part) gu = (per_part + gs - 1) / gs;  // contiguous ranges
+  const int flags = (fast ? 1 : 0) | (sc.mode << 1);
   hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kFusedThreads), lds, s, tab, a, flags, gu);
   return hipGetLastError();
 }
