@@ -454,27 +454,72 @@ __device__ __forceinline__ void mfma_slots(typename Mfma<TS>::Acc (&acc)[kGP], c
   }
 }
 
-// Add the wave's partial counts into c (upper triangle, integer atomics).
-// The lane index is passed through an empty asm statement so that the
-// compiler cannot hoist the addresses of all the atomics out of the unit loop
-// (it would keep them live in registers for the whole kernel).
+// Add the counts of one pair slot (row tile I, column tile J) into c (upper
+// triangle).  With pair64, two neighbouring counters go in one 64-bit atomic
+// add: their sum never carries across the halves because every count of a
+// layer stays below 2^32.  Direct entries (I <= J) pair neighbouring
+// columns, held by lanes l and l ^ 1; transposed entries (I > J, stored at
+// c[col][row]) pair neighbouring rows, held by registers r and r + 1 of one
+// lane.  A diagonal tile pair holds every pair of its experts twice; the
+// entries below the diagonal are dropped.
 template <int TS>
-__device__ __forceinline__ void mfma_flush(const typename Mfma<TS>::Acc (&acc)[kGP], const WaveTiles& wt, uint32_t* c,
-                                           int E, int lane_in) {
-  int lane = lane_in;
-  asm volatile("" : "+v"(lane));
-#pragma unroll
-  for (int p = 0; p < kGP; ++p) {
-    if (!(wt.act & (1 << p))) continue;
-    const int I = wt.tile[slot_a(p)], J = wt.tile[slot_b(p)];
+__device__ __forceinline__ void flush_slot(const typename Mfma<TS>::Acc& acc, int I, int J, uint32_t* c, int E,
+                                           int lane, bool pair64) {
+  const int gj = TS * J + Mfma<TS>::col(lane);
+  if (!pair64) {
 #pragma unroll
     for (int r = 0; r < Mfma<TS>::kRegs; ++r) {
       const int gi = TS * I + Mfma<TS>::row(r, lane);
-      const int gj = TS * J + Mfma<TS>::col(lane);
-      const uint32_t v = (uint32_t)acc[p][r];  // an exact integer count
-      // a diagonal tile pair holds every pair of its experts twice; keep one
+      const uint32_t v = (uint32_t)acc[r];  // an exact integer count
       const bool keep = (I != J || gi <= gj) && gi < E && gj < E && v != 0u;
       if (keep) atomicAdd(&c[(int64_t)min(gi, gj) * E + max(gi, gj)], v);
+    }
+    return;
+  }
+  u64* c64 = reinterpret_cast<u64*>(c);
+  if (I > J) {
+#pragma unroll
+    for (int r = 0; r < Mfma<TS>::kRegs; r += 2) {
+      const int gi = TS * I + Mfma<TS>::row(r, lane);  // even; row(r + 1) = gi + 1
+      const u64 v = (u64)(uint32_t)acc[r] | ((u64)(uint32_t)acc[r + 1] << 32);
+      if (gi < E && gj < E && v != 0ull) atomicAdd(&c64[((int64_t)gj * E + gi) >> 1], v);
+    }
+  } else {
+    const bool even = (lane & 1) == 0;
+#pragma unroll
+    for (int r = 0; r < Mfma<TS>::kRegs; ++r) {
+      const int gi = TS * I + Mfma<TS>::row(r, lane);
+      uint32_t v = (uint32_t)acc[r];
+      if (I == J && gi > gj) v = 0u;
+      const uint32_t w = (uint32_t)__shfl_xor((int)v, 1);  // column gj ^ 1
+      const u64 pv = even ? ((u64)v | ((u64)w << 32)) : 0ull;
+      if (gi < E && gj < E && pv != 0ull) atomicAdd(&c64[((int64_t)gi * E + gj) >> 1], pv);
+    }
+  }
+}
+
+// Add the wave's partial counts into c.  Blocks start at different pair
+// slots (rot), so that at the end of a launch, when every block flushes at
+// once, fewer of them add into the same counters at the same time.  The
+// lane index is passed through an empty asm statement so that the compiler
+// cannot hoist the addresses of all the atomics out of the unit loop (it
+// would keep them live in registers for the whole kernel).
+template <int TS>
+__device__ __forceinline__ void mfma_flush(const typename Mfma<TS>::Acc (&acc)[kGP], const WaveTiles& wt, uint32_t* c,
+                                           int E, int lane_in, int rot, bool pair64) {
+  int lane = lane_in;
+  asm volatile("" : "+v"(lane));
+  for (int t = 0; t < kGP; ++t) {
+    int p = t + rot;
+    p = p >= kGP ? p - kGP : p;
+    if (!(wt.act & (1 << p))) continue;
+    const int I = wt.tile[slot_a(p)], J = wt.tile[slot_b(p)];
+    switch (p) {  // wave-uniform: static register indices in every case
+      case 0: flush_slot<TS>(acc[0], I, J, c, E, lane, pair64); break;
+      case 1: flush_slot<TS>(acc[1], I, J, c, E, lane, pair64); break;
+      case 2: flush_slot<TS>(acc[2], I, J, c, E, lane, pair64); break;
+      case 3: flush_slot<TS>(acc[3], I, J, c, E, lane, pair64); break;
+      default: flush_slot<TS>(acc[4], I, J, c, E, lane, pair64); break;
     }
   }
 }
@@ -702,6 +747,8 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
   // consecutive units of one layer and issued together, so each expert row
   // receives 64 * SB::kUnits contiguous bytes at once (fewer read/write
   // turnarounds in HBM than one 64-byte piece per unit).  Only for E <= 256.
+  // Whole-vector stores carry the non-temporal hint: the signatures are not
+  // read again by this kernel.
   auto batch_flush = [&]() __attribute__((always_inline)) {
     if (sb_n == 0) return;
     const int e_lo = (wave * E) >> 3, e_hi = ((wave + 1) * E) >> 3;
@@ -712,7 +759,7 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
         u64* dst = sb_lb + (int64_t)(item >> 2) * a.W + sb_w0 + (item & 3) * 2;
 #pragma unroll
         for (int j = 0; j < SB::kUnits; ++j)
-          if (j < sb_n) *reinterpret_cast<v2u64*>(dst + 8 * j) = sreg[j][i];
+          if (j < sb_n) __builtin_nontemporal_store(sreg[j][i], reinterpret_cast<v2u64*>(dst + 8 * j));
       }
     }
     sb_n = 0;
@@ -759,7 +806,7 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
         const u64 wa = pbt[s0 * EPW + (e ^ bt_swz(s0))];
         const u64 wb = pbt[(s0 + 1) * EPW + (e ^ bt_swz(s0 + 1))];
         if (s0 + 1 < pend.cnt && plain(s0) && plain(s0 + 1)) {
-          *reinterpret_cast<v2u64*>(pend.lb + (int64_t)e * a.W + pend.w0 + s0) = v2u64{wa, wb};
+          __builtin_nontemporal_store(v2u64{wa, wb}, reinterpret_cast<v2u64*>(pend.lb + (int64_t)e * a.W + pend.w0 + s0));
         } else {
           put(e, s0, wa);
           if (s0 + 1 < pend.cnt) put(e, s0 + 1, wb);
@@ -777,11 +824,13 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
     if (GM == kGramMfma) mfma_slots<GS::TS>(acc, wt, pbt, EPW, s0, s1, lane);
     if (GM == kGramPopc) pg.accumulate(pbt, s0, min(s1, pend.cnt), EPW);
   };
+  // 64-bit atomics need even E (8-byte aligned rows) and an 8-byte aligned matrix
+  const bool pair64 = (E & 1) == 0 && (reinterpret_cast<uintptr_t>(a.cacc) & 7) == 0;
   auto flush = [&](int layer) {
     if (GM == kGramNone) return;
     uint32_t* cl = a.cacc + (int64_t)layer * a.cacc_layer_elems;
     if (GM == kGramMfma) {
-      mfma_flush<GS::TS>(acc, wt, cl, E, lane);
+      mfma_flush<GS::TS>(acc, wt, cl, E, lane, (int)(blockIdx.x % kGP), pair64);
       zero_acc();
     }
     if (GM == kGramPopc) {

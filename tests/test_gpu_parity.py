@@ -241,6 +241,22 @@ def test_determinism_bit_identical_reruns(dl, syn):
     assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1]) and torch.equal(a[2], b[2])
 
 
+@pytest.mark.parametrize("E,k,dtype", [(64, 6, 1), (256, 8, 0), (130, 8, 0)])
+def test_fused_distances_not_8_byte_aligned(dl, orc, syn, E, k, dtype):
+    """D only 4-byte aligned: the co-occurrence counts take 32-bit atomics."""
+    L, N = 3, 3001
+    x = np.stack([syn.normal(500 + 3 * E + l, N, E, dtype) for l in range(L)])
+    xd = to_dev(x)
+    big = torch.empty(L * E * E + 1, dtype=torch.int32, device="cuda")
+    D = big[1:].view(L, E, E)
+    assert D.data_ptr() % 8 == 4
+    bits, D, out = dl.do_fused(xd, k, want_bits=True, D=D)
+    torch.cuda.synchronize()
+    recs = dl.loss_records(out)
+    for l in range(L):
+        _check_layer(dl, orc, x[l], k, bits[l], D[l], recs[l], f"layer {l}")
+
+
 # ---------------------------------------------------------------------------
 # streaming history
 # ---------------------------------------------------------------------------
