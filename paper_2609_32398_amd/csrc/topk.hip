@@ -68,6 +68,9 @@ __device__ __forceinline__ int bt_swz(int s) { return (s & 7) << 2; }
 // the read-once stream ages out of L2 before the partially written signature
 // lines, which then merge there into whole lines before eviction.
 constexpr int kStreamPolicy = 2;
+// Fourth word of a raw buffer resource on gfx9-family GPUs (no format
+// conversion, no swizzle; offsets in bytes).
+constexpr int kBufWord3 = 0x00020000;
 // Units of signature stores held in registers (see batch_flush), and the
 // (expert, word pair) items a lane holds per unit: 4 * E/8 items per wave.
 template <int EPW>
@@ -649,19 +652,37 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
 
   // Direct-to-LDS load of full 128-byte chunk c_ of the 64 rows starting at
   // token t0_ of segment sg (asynchronous; the consumer waits with DOL_WAIT_VMEM).
+  // Rows r = 8 j + lane/8 of the 64 starting at token t0_ that lie inside the
+  // segment: [r_lo, r_hi) (wave-uniform, 32-bit compares per lane).
+  const int row_in_j0 = lane >> 3;
+  auto row_bounds = [&](const Seg& sg, int64_t t0_, int& r_lo, int& r_hi) {
+    r_lo = (int)min((int64_t)64, max((int64_t)0, -t0_));
+    r_hi = (int)max((int64_t)0, min((int64_t)64, sg.n - t0_));
+  };
+  // Direct-to-LDS load of full 128-byte chunk c_ of the 64 rows starting at
+  // token t0_ of segment sg (asynchronous; the consumer waits with
+  // DOL_WAIT_VMEM).  When every row lies inside the segment the loads go
+  // through a buffer resource based at the chunk's row 0: the row offsets are
+  // scalar and the lane offset is one 32-bit register, so issuing a load
+  // costs no vector instruction.
   auto dma = [&](const Seg& sg, int64_t t0_, int c_, unsigned char* sbuf) {
     if (c_ * 8 + 8 > rowv) return;
     const unsigned char* cbase = sg.base + t0_ * rowB + c_ * 128;  // row 0 of the chunk (uniform)
     if (t0_ >= 0 && t0_ + 64 <= sg.n) {  // every row inside the segment
+      const __amdgpu_buffer_rsrc_t rs =
+          __builtin_amdgcn_make_buffer_rsrc(const_cast<unsigned char*>(cbase), (short)0, 0x7FFFFFFF, kBufWord3);
 #pragma unroll
       for (int j = 0; j < 8; ++j)
-        __builtin_amdgcn_global_load_lds(cbase + (uint32_t)(j * 8 * rowB) + ((j & 1) ? off_odd : off_even),
-                                         (__attribute__((address_space(3))) void*)(sbuf + j * 1024), 16, 0, kStreamPolicy);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)(sbuf + j * 1024), 16,
+                                                 (j & 1) ? off_odd : off_even, (uint32_t)(j * 8 * rowB), 0,
+                                                 kStreamPolicy);
     } else {
+      int r_lo, r_hi;
+      row_bounds(sg, t0_, r_lo, r_hi);
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        const int64_t tr = t0_ + 8 * j + (lane >> 3);
-        if (tr >= 0 && tr < sg.n)
+        const int r = 8 * j + row_in_j0;
+        if (r >= r_lo && r < r_hi)
           __builtin_amdgcn_global_load_lds(cbase + (uint32_t)(j * 8 * rowB) + ((j & 1) ? off_odd : off_even),
                                            (__attribute__((address_space(3))) void*)(sbuf + j * 1024), 16, 0, kStreamPolicy);
       }
@@ -672,12 +693,14 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
   auto fill_partial = [&](const Seg& sg, int64_t t0_, int c_, unsigned char* sbuf) {
     const int cvn = rowv - c_ * 8;
     const unsigned char* cbase = sg.base + t0_ * rowB + c_ * 128;
+    int r_lo, r_hi;
+    row_bounds(sg, t0_, r_lo, r_hi);
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      const int64_t tr = t0_ + 8 * j + (lane >> 3);
+      const int r = 8 * j + row_in_j0;
       const int q = q_even ^ (j & 1);
       v4u val = v4u{~0u, ~0u, ~0u, ~0u};
-      if (q < cvn && tr >= 0 && tr < sg.n)
+      if (q < cvn && r >= r_lo && r < r_hi)
         val = *reinterpret_cast<const v4u*>(cbase + (uint32_t)(j * 8 * rowB) + ((j & 1) ? off_odd : off_even));
       *reinterpret_cast<v4u*>(sbuf + j * 1024 + lane * 16) = val;
     }
@@ -773,20 +796,26 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
         sb_lb = pend.lb;
         sb_w0 = pend.w0;
       }
-      v2u64 v[SB::kItems];
+      // load this unit's items straight into batch slot sb_n: a branch per
+      // slot (wave-uniform) with static register indices, instead of a
+      // select over every slot
+      auto load_into = [&](v2u64 (&dst)[SB::kItems]) __attribute__((always_inline)) {
+        DOL_WAVE_FENCE();  // keeps the loads inside their branch
 #pragma unroll
-      for (int i = 0; i < SB::kItems; ++i) {
-        const int item = e_lo * 4 + lane + i * kWave;
-        const int e = item >> 2, s0 = (item & 3) * 2;
-        v[i] = item < e_hi * 4 ? v2u64{pbt[s0 * EPW + (e ^ bt_swz(s0))], pbt[(s0 + 1) * EPW + (e ^ bt_swz(s0 + 1))]}
-                               : v2u64{0ull, 0ull};
-      }
-#pragma unroll
-      for (int j = 0; j < SB::kUnits; ++j)
-        if (j == sb_n) {
-#pragma unroll
-          for (int i = 0; i < SB::kItems; ++i) sreg[j][i] = v[i];
+        for (int i = 0; i < SB::kItems; ++i) {
+          const int item = e_lo * 4 + lane + i * kWave;
+          const int e = item >> 2, s0 = (item & 3) * 2;
+          dst[i] = item < e_hi * 4
+                       ? v2u64{pbt[s0 * EPW + (e ^ bt_swz(s0))], pbt[(s0 + 1) * EPW + (e ^ bt_swz(s0 + 1))]}
+                       : v2u64{0ull, 0ull};
         }
+      };
+      switch (sb_n) {
+        case 0: load_into(sreg[0]); break;
+        case 1: load_into(sreg[1 % SB::kUnits]); break;
+        case 2: load_into(sreg[2 % SB::kUnits]); break;
+        default: load_into(sreg[3 % SB::kUnits]); break;
+      }
       if (++sb_n == SB::kUnits) batch_flush();
       return;
     }
