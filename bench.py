@@ -242,7 +242,7 @@ def bench_layers(args, cfg):
         data="synthetic",
         config=dict(workload=w["name"], layers=L, tokens_per_layer=N, experts=E, k=k,
                     score_dtype="f32" if w["dtype"] == 0 else "bf16", signatures_written=True),
-        roofline=roofline(alg_bytes, kern_ms, w["name"], "k_topk (fused top-k, signatures, int8 MFMA Gram)",
+        roofline=roofline(alg_bytes, kern_ms, w["name"], "k_topk (fused top-k, signatures, fp4 MFMA Gram)",
                           bytes_per_token),
         step_gbs=alg_bytes / (ms_per_step / 1e3) / 1e9,
         without_signature_output=dict(kernel_ms=nb_ms, algorithmic_bytes=nb_bytes,

@@ -796,26 +796,20 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
         sb_lb = pend.lb;
         sb_w0 = pend.w0;
       }
-      // load this unit's items straight into batch slot sb_n: a branch per
-      // slot (wave-uniform) with static register indices, instead of a
-      // select over every slot
-      auto load_into = [&](v2u64 (&dst)[SB::kItems]) __attribute__((always_inline)) {
-        DOL_WAVE_FENCE();  // keeps the loads inside their branch
+      v2u64 v[SB::kItems];
 #pragma unroll
-        for (int i = 0; i < SB::kItems; ++i) {
-          const int item = e_lo * 4 + lane + i * kWave;
-          const int e = item >> 2, s0 = (item & 3) * 2;
-          dst[i] = item < e_hi * 4
-                       ? v2u64{pbt[s0 * EPW + (e ^ bt_swz(s0))], pbt[(s0 + 1) * EPW + (e ^ bt_swz(s0 + 1))]}
-                       : v2u64{0ull, 0ull};
-        }
-      };
-      switch (sb_n) {
-        case 0: load_into(sreg[0]); break;
-        case 1: load_into(sreg[1 % SB::kUnits]); break;
-        case 2: load_into(sreg[2 % SB::kUnits]); break;
-        default: load_into(sreg[3 % SB::kUnits]); break;
+      for (int i = 0; i < SB::kItems; ++i) {
+        const int item = e_lo * 4 + lane + i * kWave;
+        const int e = item >> 2, s0 = (item & 3) * 2;
+        v[i] = item < e_hi * 4 ? v2u64{pbt[s0 * EPW + (e ^ bt_swz(s0))], pbt[(s0 + 1) * EPW + (e ^ bt_swz(s0 + 1))]}
+                               : v2u64{0ull, 0ull};
       }
+#pragma unroll
+      for (int j = 0; j < SB::kUnits; ++j)
+        if (j == sb_n) {
+#pragma unroll
+          for (int i = 0; i < SB::kItems; ++i) sreg[j][i] = v[i];
+        }
       if (++sb_n == SB::kUnits) batch_flush();
       return;
     }
