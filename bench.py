@@ -199,7 +199,8 @@ def bench_layers(args, cfg):
     for a, b in nb:
         a.record()
         b.record()
-    dl.do_fused(scores, k, D=D, out=out)
+    for _ in range(max(args.warmup, 3)):  # the library settles this launch shape's schedule here
+        dl.do_fused(scores, k, D=D, out=out)
     torch.cuda.synchronize()
     for a, b in nb:
         dl.do_profile_next(a, b)

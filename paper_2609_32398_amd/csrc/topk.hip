@@ -35,7 +35,10 @@
 // popcount(a & b) on 4x4 micro-tiles per thread.  Either way a block adds its
 // integer partial counts into the accumulator matrix when the layer changes
 // and at the end (order-independent).
+#include <algorithm>
+#include <cstdio>
 #include <cstdlib>
+#include <mutex>
 
 #include "common.h"
 
@@ -1035,8 +1038,8 @@ int gram_mode() {
   return g_gram_mode;
 }
 
-// Unit schedule of the Top-K kernel.  gu < 0: chosen per launch (below);
-// DOLOSS_SCHED overrides it for tuning: "c" = one contiguous range per
+// Unit schedule of the Top-K kernel.  gu < 0: chosen per launch
+// (tuned_schedule); DOLOSS_SCHED fixes it instead: "c" = one contiguous range per
 // block, "i<n>" / "x<n>" / "p<n>" = groups of n units in placement mode 0 / 1
 // / 2 (see k_topk).
 struct Sched {
@@ -1059,7 +1062,7 @@ Sched schedule() {
 }
 
 template <typename T, int EP, int GM>
-hipError_t launch_one(const SegTable& tab, const PathArgs& a, bool fast, hipStream_t s) {
+hipError_t launch_one(const SegTable& tab, const PathArgs& a, bool fast, Sched sc, hipStream_t s) {
   constexpr int EPW = EP < 32 ? 32 : EP;
   auto kern = k_topk<T, EP, GM>;
   const size_t lds = (fast ? (size_t)kStageBytes : 0) + 2 * (size_t)kFusedWaves * EPW * sizeof(u64);
@@ -1072,13 +1075,6 @@ hipError_t launch_one(const SegTable& tab, const PathArgs& a, bool fast, hipStre
   const int64_t units = tab.tile_start[tab.nseg];
   int64_t blocks = std::min<int64_t>((int64_t)di.cu_count * occ, units);
   blocks = std::max<int64_t>(blocks, 1);
-  // Interleaved groups of 4 units with XCD-adjacent placement keep the
-  // signature stores of all blocks side by side; a block then changes output
-  // layer at every group, so that schedule is used only when every layer
-  // spans several rounds of groups (or the launch has one output layer).
-  // Default: eight XCD partitions, groups of 4 units (placement mode 2).
-  Sched sc = schedule();
-  if (sc.gu < 0) sc = Sched{4, 2};
   int64_t gu = sc.gu;
   const int64_t per_part = sc.mode == 2 ? (units + 7) / 8 : units;
   const int64_t gs = sc.mode == 2 ? std::max<int64_t>(blocks / 8, 1) : blocks;
@@ -1089,23 +1085,134 @@ hipError_t launch_one(const SegTable& tab, const PathArgs& a, bool fast, hipStre
 }
 
 template <typename T, int EP>
-hipError_t launch_gm(const SegTable& tab, const PathArgs& a, bool fast, hipStream_t s) {
-  if (a.cacc == nullptr) return launch_one<T, EP, kGramNone>(tab, a, fast, s);
-  if (gram_mode() == kGramPopc) return launch_one<T, EP, kGramPopc>(tab, a, fast, s);
-  return launch_one<T, EP, kGramMfma>(tab, a, fast, s);
+hipError_t launch_gm(const SegTable& tab, const PathArgs& a, bool fast, Sched sc, hipStream_t s) {
+  if (a.cacc == nullptr) return launch_one<T, EP, kGramNone>(tab, a, fast, sc, s);
+  if (gram_mode() == kGramPopc) return launch_one<T, EP, kGramPopc>(tab, a, fast, sc, s);
+  return launch_one<T, EP, kGramMfma>(tab, a, fast, sc, s);
 }
 
 template <typename T>
-hipError_t launch_ep(const SegTable& tab, const PathArgs& a, bool fast, hipStream_t s) {
+hipError_t launch_ep(const SegTable& tab, const PathArgs& a, bool fast, Sched sc, hipStream_t s) {
   const int E = a.E;
-  if (E <= 32) return launch_gm<T, 32>(tab, a, fast, s);
-  if (E <= 64) return launch_gm<T, 64>(tab, a, fast, s);
-  if (E <= 128) return launch_gm<T, 128>(tab, a, fast, s);
-  if (E <= 256) return launch_gm<T, 256>(tab, a, fast, s);
+  if (E <= 32) return launch_gm<T, 32>(tab, a, fast, sc, s);
+  if (E <= 64) return launch_gm<T, 64>(tab, a, fast, sc, s);
+  if (E <= 128) return launch_gm<T, 128>(tab, a, fast, sc, s);
+  if (E <= 256) return launch_gm<T, 256>(tab, a, fast, sc, s);
   // E in (256, 1024]: exact per-lane selection, signatures only
   if (a.cacc != nullptr) return hipErrorInvalidValue;
-  if (E <= 512) return launch_one<T, 512, kGramNone>(tab, a, false, s);
-  return launch_one<T, 1024, kGramNone>(tab, a, false, s);
+  if (E <= 512) return launch_one<T, 512, kGramNone>(tab, a, false, sc, s);
+  return launch_one<T, 1024, kGramNone>(tab, a, false, sc, s);
+}
+
+// Launch-time choice of the unit schedule for large launches.  The cost of
+// the signature stores under a given schedule differs between otherwise
+// identical boards (it follows how the concurrent store streams fall on
+// the HBM channels), while it repeats within one process.  So for each
+// large launch shape the first launches try the candidates with events
+// around them; completed measurements are collected with hipEventQuery,
+// which never waits, and once every candidate has one, the fastest is used
+// for all later launches of that shape.  The very first launch of a shape is
+// not measured (cold caches and TLB).  Launches under stream capture and
+// launches below kTuneMinUnits use the first candidate.
+constexpr Sched kSchedCand[2] = {Sched{4, 2}, Sched{0, 0}};  // XCD partitions; contiguous ranges
+constexpr int kNumCand = 2;
+constexpr int64_t kTuneMinUnits = 8192;  // 4 Mi tokens
+constexpr int kTuneSlots = 16;
+
+struct Tune {
+  uint64_t key;
+  int device;
+  int calls;
+  int chosen;                 // index into kSchedCand, or -1 while measuring
+  float best[kNumCand];       // fastest completed launch per candidate (ms), < 0 if none yet
+  bool pending[kNumCand];     // a measured launch is in flight
+  hipEvent_t ev[kNumCand][2];
+};
+std::mutex g_tune_mu;
+Tune g_tune[kTuneSlots];
+int g_ntune = 0;
+
+uint64_t mix(uint64_t h, uint64_t v) {
+  h ^= v + 0x9E3779B97F4A7C15ull + (h << 6) + (h >> 2);
+  return h;
+}
+
+// Picks the schedule of one launch and, when it is a measured trial, sets
+// *ev_out to the candidate's start/stop events.
+Sched tuned_schedule(do_dtype dt, const SegTable& tab, const PathArgs& a, bool fast, hipStream_t s,
+                     hipEvent_t* ev_out) {
+  ev_out[0] = ev_out[1] = nullptr;
+  const int64_t units = tab.tile_start[tab.nseg];
+  if (units < kTuneMinUnits) return kSchedCand[0];
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  const bool capturing = hipStreamIsCapturing(s, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return kSchedCand[0];
+  uint64_t key = 0;
+  key = mix(key, (uint64_t)dt);
+  key = mix(key, (uint64_t)a.E);
+  key = mix(key, (uint64_t)a.k);
+  key = mix(key, (uint64_t)units);
+  key = mix(key, (uint64_t)tab.nseg);
+  key = mix(key, (uint64_t)tab.s[tab.nseg - 1].layer - (uint64_t)tab.s[0].layer);
+  key = mix(key, (uint64_t)(a.bits != nullptr) | ((uint64_t)(a.cacc != nullptr) << 1) |
+                     ((uint64_t)a.or_partial << 2) | ((uint64_t)fast << 3));
+  std::lock_guard<std::mutex> lock(g_tune_mu);
+  Tune* t = nullptr;
+  for (int i = 0; i < g_ntune; ++i)
+    if (g_tune[i].key == key && g_tune[i].device == dev) t = &g_tune[i];
+  if (t == nullptr) {
+    if (g_ntune == kTuneSlots) return kSchedCand[0];
+    t = &g_tune[g_ntune++];
+    *t = Tune{};
+    t->key = key;
+    t->device = dev;
+    t->chosen = -1;
+    for (int c = 0; c < kNumCand; ++c) t->best[c] = -1.f;
+  }
+  if (t->chosen >= 0) return kSchedCand[t->chosen];
+  // collect finished trials
+  bool all = true;
+  for (int c = 0; c < kNumCand; ++c) {
+    if (t->pending[c]) {
+      const hipError_t q = hipEventQuery(t->ev[c][1]);
+      if (q == hipSuccess) {
+        float ms = -1.f;
+        if (hipEventElapsedTime(&ms, t->ev[c][0], t->ev[c][1]) == hipSuccess && ms > 0.f)
+          t->best[c] = t->best[c] < 0.f ? ms : std::min(t->best[c], ms);
+        t->pending[c] = false;
+      } else if (q != hipErrorNotReady) {
+        t->chosen = 0;  // measurement failed: keep the first candidate
+        return kSchedCand[0];
+      }
+    }
+    all = all && t->best[c] > 0.f;
+  }
+  if (all) {
+    int bc = 0;
+    for (int c = 1; c < kNumCand; ++c)
+      if (t->best[c] < 0.97f * t->best[bc]) bc = c;  // switch only for a clear gain
+    t->chosen = bc;
+    if (getenv("DOLOSS_TUNE_LOG") != nullptr)
+      fprintf(stderr, "[doloss] unit schedule for %lld units: candidates %.4f / %.4f ms, chose %d\n",
+              (long long)units, t->best[0], t->best[1], bc);
+    return kSchedCand[bc];
+  }
+  if (capturing || t->calls++ == 0) return kSchedCand[0];
+  for (int c = 0; c < kNumCand; ++c) {
+    if (t->best[c] > 0.f || t->pending[c]) continue;
+    if (t->ev[c][0] == nullptr) {
+      if (hipEventCreate(&t->ev[c][0]) != hipSuccess || hipEventCreate(&t->ev[c][1]) != hipSuccess) {
+        t->chosen = 0;
+        return kSchedCand[0];
+      }
+    }
+    t->pending[c] = true;
+    ev_out[0] = t->ev[c][0];
+    ev_out[1] = t->ev[c][1];
+    return kSchedCand[c];
+  }
+  return kSchedCand[0];
 }
 
 }  // namespace
@@ -1120,7 +1227,16 @@ hipError_t launch_topk(do_dtype dt, SegTable& tab, int nseg, const PathArgs& a, 
   }
   if (tab.tile_start[nseg] == 0) return hipSuccess;
   const bool fast = fast_ok && a.k <= kFastMaxK && a.E <= kFastMaxE;
-  return dt == DO_F32 ? launch_ep<float>(tab, a, fast, s) : launch_ep<uint16_t>(tab, a, fast, s);
+  Sched sc = schedule();
+  hipEvent_t ev[2] = {nullptr, nullptr};
+  if (sc.gu < 0) sc = tuned_schedule(dt, tab, a, fast, s, ev);
+  if (ev[0] != nullptr) {
+    const hipError_t e = hipEventRecord(ev[0], s);
+    if (e != hipSuccess) return e;
+  }
+  const hipError_t e = dt == DO_F32 ? launch_ep<float>(tab, a, fast, sc, s) : launch_ep<uint16_t>(tab, a, fast, sc, s);
+  if (e != hipSuccess || ev[1] == nullptr) return e;
+  return hipEventRecord(ev[1], s);
 }
 
 }  // namespace dol
