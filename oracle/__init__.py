@@ -15,6 +15,8 @@ computes, written from the paper's definitions (arXiv 2609.32398):
 * ``surrogate``       -- Sec. 3.1.3, Eq. (6)-(7): the surrogate loss
   (scale/(N^2 k)) sum_ij G_ij C_ij, C_ij = sum_t p_it (f_it - f_jt), and its
   gradient with respect to the routing probabilities (G, F detached).
+* ``load_stats``      -- per-expert loads n_i (App. C.3), the Local-LBL loss
+  sum_i f_i P_i of Sec. 4.2 and MaxVio (App. E) over a rank placement.
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 ``bench.py`` may use this package.  It shares no code with the HIP library.
@@ -38,6 +40,11 @@ F32, BF16 = 0, 1
 class _LossResult(ctypes.Structure):
     _fields_ = [("sum", ctypes.c_uint64), ("sumsq", ctypes.c_uint64), ("loss", ctypes.c_double),
                 ("mean", ctypes.c_double), ("var", ctypes.c_double)]
+
+
+class _LoadStatsResult(ctypes.Structure):
+    _fields_ = [("total", ctypes.c_uint64), ("max_load", ctypes.c_uint32), ("min_load", ctypes.c_uint32),
+                ("lbl", ctypes.c_double), ("maxvio", ctypes.c_double)]
 
 
 def build(force: bool = True) -> str:
@@ -65,7 +72,10 @@ def _load():
         lib.oracle_loss.argtypes = [vp, i32, ctypes.POINTER(_LossResult)]
         lib.oracle_surrogate.argtypes = [vp, ctypes.c_int, i64, i32, i32, vp, vp, ctypes.c_double,
                                          ctypes.POINTER(ctypes.c_double), vp, ctypes.c_int]
-        for f in ("oracle_topk_signature", "oracle_pack", "oracle_hamming", "oracle_loss", "oracle_surrogate"):
+        lib.oracle_load_stats.argtypes = [vp, i64, i32, i32, vp, ctypes.c_int, vp, i32, vp,
+                                          ctypes.POINTER(_LoadStatsResult)]
+        for f in ("oracle_topk_signature", "oracle_pack", "oracle_hamming", "oracle_loss", "oracle_surrogate",
+                  "oracle_load_stats"):
             getattr(lib, f).restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -146,6 +156,30 @@ def surrogate(p: np.ndarray, F: np.ndarray, G: np.ndarray, k: int, scale: float 
     if rc:
         raise ValueError(f"oracle_surrogate: bad arguments N={N} E={E} k={k}")
     return float(loss.value), grad
+
+
+def load_stats(F: np.ndarray, k: int, p: np.ndarray | None = None, rank=None, R: int = 0):
+    """Loads n_i, Local-LBL and MaxVio of F[E][N] (p of shape (N, E) or None;
+    rank: expert -> rank list/array or None for one expert per rank).
+    Returns (loads uint32[E], dict)."""
+    F = np.ascontiguousarray(F, dtype=np.uint8)
+    E, N = F.shape
+    loads = np.empty(E, dtype=np.uint32)
+    pp = None
+    dt = F32
+    if p is not None:
+        pp = np.ascontiguousarray(p)
+        assert pp.shape == (N, E)
+        dt = _dtype_of(pp)
+    rk = None if rank is None else np.ascontiguousarray(rank, dtype=np.int32)
+    r = _LoadStatsResult()
+    rc = _load().oracle_load_stats(F.ctypes.data, N, E, k, pp.ctypes.data if pp is not None else None, dt,
+                                   rk.ctypes.data if rk is not None else None, R, loads.ctypes.data,
+                                   ctypes.byref(r))
+    if rc:
+        raise ValueError(f"oracle_load_stats: bad arguments N={N} E={E} k={k} R={R}")
+    return loads, dict(total=int(r.total), max_load=int(r.max_load), min_load=int(r.min_load),
+                       lbl=float(r.lbl), maxvio=float(r.maxvio))
 
 
 def run(scores: np.ndarray, k: int, nthreads: int | None = None):

@@ -27,6 +27,10 @@
  *                          C_ij = sum_t p_it (f_it - f_jt) written out, and its
  *                          gradient with respect to the routing probabilities
  *                          p with G and F held constant.
+ *   oracle_load_stats      per-expert loads n_i = ||F_i||_1 (App. C.3), the
+ *                          Local-LBL balance loss sum_i f_i P_i of Sec. 4.2 and
+ *                          the MaxVio imbalance of App. E over a placement of
+ *                          the experts on ranks.
  *
  * Readings where the paper is silent (each listed in the design notes):
  *   - ties in Top-K go to the lower expert index;
@@ -204,5 +208,78 @@ int oracle_surrogate(const void* p, int dtype, int64_t N, int32_t E, int32_t k, 
         grad[t * E + i] = norm * g;
       }
   }
+  return 0;
+}
+
+/*
+ * Load statistics of one layer's assignments F[E][N] (App. C.3, Sec. 4.2,
+ * App. E).
+ *   loads[i]  n_i = sum_t f_it, the number of tokens routed to expert i.
+ *   lbl       Local-LBL sum_i f_i P_i with f_i = n_i / (N k), the fraction of
+ *             the N k routing assignments that go to expert i, and
+ *             P_i = (1/N) sum_t p_it, the mean routing probability; 0 when p
+ *             is NULL.
+ *   maxvio    max over ranks r of |L_r / tau - 1|, L_r the summed load of the
+ *             experts placed on rank r (rank[i], R ranks; NULL: every expert
+ *             its own rank), tau the mean of the L_r; 0 when tau is 0.
+ * Returns -1 on bad arguments (including a rank outside [0, R)).
+ */
+typedef struct {
+  uint64_t total;
+  uint32_t max_load, min_load;
+  double lbl;
+  double maxvio;
+} oracle_load_stats_result;
+
+int oracle_load_stats(const uint8_t* F, int64_t N, int32_t E, int32_t k, const void* p, int dtype,
+                      const int32_t* rank, int32_t R, uint32_t* loads, oracle_load_stats_result* out) {
+  if (N < 1 || E < 1 || k < 1 || k > E) return -1;
+  if (rank == NULL) R = E;
+  if (R < 1) return -1;
+  uint64_t total = 0;
+  uint32_t mx = 0, mn = 0xFFFFFFFFu;
+  for (int32_t i = 0; i < E; ++i) {
+    uint64_t n = 0;
+    for (int64_t t = 0; t < N; ++t) n += F[(int64_t)i * N + t];
+    loads[i] = (uint32_t)n;
+    total += n;
+    if ((uint32_t)n > mx) mx = (uint32_t)n;
+    if ((uint32_t)n < mn) mn = (uint32_t)n;
+  }
+  double lbl = 0.0;
+  if (p != NULL) {
+    for (int32_t i = 0; i < E; ++i) {
+      double P = 0.0;
+      for (int64_t t = 0; t < N; ++t) P += score_at(p, dtype, t * E + i);
+      P /= (double)N;
+      const double f = (double)loads[i] / ((double)N * (double)k);
+      lbl += f * P;
+    }
+  }
+  double* Lr = (double*)calloc((size_t)R, sizeof(double));
+  if (!Lr) return -2;
+  for (int32_t i = 0; i < E; ++i) {
+    const int32_t r = rank ? rank[i] : i;
+    if (r < 0 || r >= R) {
+      free(Lr);
+      return -1;
+    }
+    Lr[r] += (double)loads[i];
+  }
+  double tau = 0.0;
+  for (int32_t r = 0; r < R; ++r) tau += Lr[r];
+  tau /= (double)R;
+  double mv = 0.0;
+  if (tau > 0.0)
+    for (int32_t r = 0; r < R; ++r) {
+      const double v = fabs(Lr[r] / tau - 1.0);
+      if (v > mv) mv = v;
+    }
+  free(Lr);
+  out->total = total;
+  out->max_load = mx;
+  out->min_load = mn;
+  out->lbl = lbl;
+  out->maxvio = mv;
   return 0;
 }
