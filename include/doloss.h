@@ -139,6 +139,37 @@ do_status do_fused(const void* scores, do_dtype dtype, int64_t N, int32_t E, int
 do_status do_surrogate(const void* p, do_dtype dtype, int64_t N, int32_t E, int32_t k, int32_t L, const uint64_t* bits,
                        const uint32_t* D, double scale, double* loss, float* grad, hipStream_t stream);
 
+/* Per-layer load statistics (device memory, 32 bytes). */
+typedef struct {
+  uint64_t total;    /* sum_i n_i: N*k for Top-K signatures */
+  uint32_t max_load; /* max_i n_i */
+  uint32_t min_load; /* min_i n_i */
+  double lbl;        /* Local-LBL (Sec. 4.2) sum_i f_i P_i, f_i = n_i / (N k), P_i = (1/N) sum_t p_it; 0 without p */
+  double maxvio;     /* App. E: max over ranks r of |L_r / tau - 1|, tau the mean rank load; 0 if tau is 0 */
+} do_load_stats_result;
+
+/*
+ * Load statistics of signatures: the per-expert loads n_i = ||F_i||_1 (the
+ * diagonal of the co-occurrence counts, App. C.3), the Local-LBL balance loss
+ * of Sec. 4.2 and the MaxVio imbalance of App. E for a placement of the
+ * experts on ranks (L_r = sum of the loads of the experts on rank r).
+ *   bits         [L][E][ld] device, ld = words per expert row (0 means
+ *                ceil(N/64); a stream history uses do_stream_words_per_expert);
+ *                bits past N must be zero
+ *   p            nullable, [L][N][E] device routing probabilities (fp32 or
+ *                bf16, aligned to the element); NULL leaves lbl at 0
+ *   expert_rank  nullable HOST array [E] of ranks in [0, R), read during the
+ *                call; NULL places every expert on its own rank (R = E)
+ *   loads        [L][E] device uint32, overwritten
+ *   out          [L] device, overwritten
+ * Limits as for do_topk_signature; 1 <= R <= 1024.  lbl is accumulated in
+ * fp64 with atomic adds, so its last bits may differ between runs; the other
+ * fields are exact and deterministic.
+ */
+do_status do_load_stats(const uint64_t* bits, int64_t N, int64_t ld, int32_t E, int32_t k, int32_t L, const void* p,
+                        do_dtype dtype, const int32_t* expert_rank, int32_t R, uint32_t* loads,
+                        do_load_stats_result* out, hipStream_t stream);
+
 /*
  * Streaming global-batch history (Sec. 3.1.4: distances over a batch wider
  * than one micro-batch; App. F.2, Table 4: G over gradient-accumulated

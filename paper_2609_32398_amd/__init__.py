@@ -30,6 +30,7 @@ DO_F32, DO_BF16 = 0, 1
 
 LOSS_RESULT_BYTES = 40
 LOSS_FIELDS = ("sum", "sumsq", "loss", "mean", "var")
+LOAD_STATS_BYTES = 32
 
 
 class DoLossError(RuntimeError):
@@ -56,6 +57,7 @@ def lib():
             "do_loss": ([vp, i32, i32, vp, vp], st),
             "do_fused": ([vp, st, i64, i32, i32, i32, vp, vp, vp, vp], st),
             "do_surrogate": ([vp, st, i64, i32, i32, i32, vp, vp, ctypes.c_double, vp, vp, vp], st),
+            "do_load_stats": ([vp, i64, i64, i32, i32, i32, vp, st, vp, i32, vp, vp, vp], st),
             "do_stream_create": ([i32, i32, i64, ctypes.POINTER(vp)], st),
             "do_stream_append": ([vp, vp, st, i64, vp], st),
             "do_stream_append_many": ([vp, ctypes.POINTER(vp), st, i64, i32, vp], st),
@@ -201,6 +203,47 @@ def do_surrogate(p: torch.Tensor, k: int, bits: torch.Tensor, D: torch.Tensor, s
                               loss.data_ptr(), grad.data_ptr() if grad is not None else None, _stream()),
            "do_surrogate")
     return loss, grad
+
+
+def do_load_stats(bits: torch.Tensor, N: int, k: int, p: torch.Tensor | None = None, expert_rank=None,
+                  R: int = 0, ld: int = 0, bits_ptr: int | None = None, E: int | None = None, L: int | None = None,
+                  loads: torch.Tensor | None = None, out: torch.Tensor | None = None):
+    """Per-expert loads (uint32 as int32 [L, E]) and per-layer statistics ([L, 32] bytes, see
+    load_stats_records) of signatures `bits` [L, E, ld or ceil(N/64)] (or a raw device pointer
+    `bits_ptr` with E and L given, e.g. a stream history).  p: routing probabilities [L, N, E] or
+    None; expert_rank: host sequence of E ranks in [0, R) or None (one expert per rank)."""
+    if bits_ptr is None:
+        if bits.dim() == 2:
+            bits = bits.unsqueeze(0)
+        L, E = bits.shape[0], bits.shape[1]
+        ptr = bits.data_ptr()
+        dev = bits.device
+    else:
+        ptr = bits_ptr
+        dev = torch.device("cuda", torch.cuda.current_device())
+    if loads is None:
+        loads = torch.empty((L, E), dtype=torch.int32, device=dev)
+    if out is None:
+        out = torch.empty((L, LOAD_STATS_BYTES), dtype=torch.uint8, device=dev)
+    rk = None
+    if expert_rank is not None:
+        rk = (ctypes.c_int32 * E)(*[int(r) for r in expert_rank])
+    pptr, pdt = (p.data_ptr(), _dtype_code(p)) if p is not None else (None, DO_F32)
+    _check(lib().do_load_stats(ptr, N, ld, E, k, L, pptr, pdt, rk, R, loads.data_ptr(), out.data_ptr(), _stream()),
+           "do_load_stats")
+    return loads, out
+
+
+def load_stats_records(out: torch.Tensor) -> list[dict]:
+    """Decode a [L, 32] uint8 tensor of do_load_stats_result records."""
+    raw = out.detach().cpu().contiguous().view(torch.uint8).numpy().reshape(-1, LOAD_STATS_BYTES)
+    recs = []
+    for r in raw:
+        u = r[8:16].view("<u4")
+        d = r[16:].view("<f8")
+        recs.append(dict(total=int(r[:8].view("<u8")[0]), max_load=int(u[0]), min_load=int(u[1]), lbl=float(d[0]),
+                         maxvio=float(d[1])))
+    return recs
 
 
 def do_profile_next(start: "torch.cuda.Event | None", stop: "torch.cuda.Event | None"):

@@ -228,6 +228,39 @@ DOLOSS_API do_status do_surrogate(const void* p, do_dtype dtype, int64_t N, int3
   return hip_status(profiled(stream, [&] { return dol::launch_surrogate(dtype, a, stream); }), "surrogate");
 }
 
+DOLOSS_API do_status do_load_stats(const uint64_t* bits, int64_t N, int64_t ld, int32_t E, int32_t k, int32_t L,
+                                   const void* p, do_dtype dtype, const int32_t* expert_rank, int32_t R,
+                                   uint32_t* loads, do_load_stats_result* out, hipStream_t stream) {
+  DO_TRY(check_shape(N, E, L));
+  DO_TRY(check_k(k, E));
+  const int64_t W = (N + 63) / 64;
+  if (ld == 0) ld = W;
+  if (ld < W) return fail(DO_ERR_INVALID_ARG, "ld must be 0 or at least ceil(N/64)");
+  if (bits == nullptr || !aligned(bits, 8)) return fail(DO_ERR_INVALID_ARG, "bits is NULL or not 8-byte aligned");
+  if (loads == nullptr || !aligned(loads, 4)) return fail(DO_ERR_INVALID_ARG, "loads is NULL or not 4-byte aligned");
+  if (out == nullptr || !aligned(out, 8)) return fail(DO_ERR_INVALID_ARG, "out is NULL or not 8-byte aligned");
+  if (p != nullptr) {
+    DO_TRY(check_dtype(dtype));
+    DO_TRY(check_scores(p, dtype));
+  }
+  dol::RankMap rm{};
+  rm.R = E;
+  rm.given = 0;
+  if (expert_rank != nullptr) {
+    if (R < 1 || R > dol::kMaxE) return fail(DO_ERR_INVALID_ARG, "R must be in [1, 1024]");
+    for (int32_t i = 0; i < E; ++i) {
+      if (expert_rank[i] < 0 || expert_rank[i] >= R)
+        return fail(DO_ERR_INVALID_ARG, "expert_rank[" + std::to_string(i) + "] is not in [0, R)");
+      rm.rank[i] = (uint16_t)expert_rank[i];
+    }
+    rm.R = R;
+    rm.given = 1;
+  }
+  return hip_status(dol::launch_load_stats(reinterpret_cast<const u64*>(bits), N, ld, E, k, L, p, dtype, rm, loads,
+                                           out, stream),
+                    "load stats");
+}
+
 DOLOSS_API do_status do_stream_create(int32_t E, int32_t k, int64_t capacity_tokens, do_stream** out) {
   if (out == nullptr) return fail(DO_ERR_INVALID_ARG, "out is NULL");
   *out = nullptr;

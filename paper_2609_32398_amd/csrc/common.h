@@ -90,6 +90,21 @@ hipError_t launch_finalize(const uint32_t* cacc, uint32_t* D, do_loss_result* ou
 // Surrogate loss (Eq. 7) and its gradient; a.loss must be zero.
 hipError_t launch_surrogate(do_dtype dt, const SurrogateArgs& a, hipStream_t s);
 
+// Expert-to-rank placement passed by value to the load-statistics finalize.
+struct RankMap {
+  uint16_t rank[kMaxE];
+  int32_t R;      // ranks; the placement is the identity (R = E) when `given` is 0
+  int32_t given;
+};
+
+// Load statistics: loads[l][e] = popcount of signature row e of layer l
+// (ld words per row, W = ceil(N/64) of them read); with p, the Local-LBL sum
+// accumulated into out[l].lbl (zeroed by the caller) and scaled in the
+// finalize, which also writes total / max / min / MaxVio.
+hipError_t launch_load_stats(const u64* bits, int64_t N, int64_t ld, int32_t E, int32_t k, int32_t L, const void* p,
+                             do_dtype dt, const RankMap& rm, uint32_t* loads, do_load_stats_result* out,
+                             hipStream_t s);
+
 // Loss of arbitrary distance matrices.
 hipError_t launch_loss(const uint32_t* D, int32_t E, int32_t L, do_loss_result* out, hipStream_t s);
 

@@ -1,0 +1,205 @@
+// Load statistics of signatures: per-expert loads (App. C.3), the Local-LBL
+// balance loss (Sec. 4.2) and the MaxVio imbalance (App. E).
+//
+//   n_i     = popcount of signature row i (the tokens routed to expert i)
+//   lbl     = sum_i f_i P_i,  f_i = n_i / (N k),  P_i = (1/N) sum_t p_it
+//           = (1 / (N^2 k)) sum_i n_i sum_t p_it
+//   maxvio  = max_r |L_r / tau - 1|,  L_r = sum of n_i over the experts on
+//             rank r,  tau = mean of the L_r
+//
+// Three launches: k_row_loads (one block per signature row, a streaming
+// popcount), k_lbl_sums (column sums of p weighted by the loads, read once;
+// only when p is given) and k_load_finalize (one block per layer).
+#include <algorithm>
+
+#include "common.h"
+
+namespace dol {
+namespace {
+
+constexpr int kLsThreads = 256;
+constexpr int kLsUnroll = 8;
+
+template <typename V>
+__device__ __forceinline__ V block_sum(V v, V* red) {
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) v += __shfl_xor(v, d);
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  if (lane == 0) red[w] = v;
+  __syncthreads();
+  V t = 0;
+  if (threadIdx.x == 0)
+    for (int i = 0; i < (int)(blockDim.x >> 6); ++i) t += red[i];
+  __syncthreads();
+  return t;  // valid in thread 0
+}
+
+// blockIdx.x = expert, blockIdx.y = layer.  Reads the W = ceil(N/64) words of
+// the row (bits past N are zero by contract).
+__global__ __launch_bounds__(kLsThreads) void k_row_loads(const u64* bits, int64_t W, int64_t ld, int32_t E,
+                                                          uint32_t* loads) {
+  __shared__ uint32_t red[kLsThreads / kWave];
+  const int e = blockIdx.x, l = blockIdx.y;
+  const u64* row = bits + ((int64_t)l * E + e) * ld;
+  uint32_t c = 0;
+  int64_t w = threadIdx.x;
+  for (; w + 3 * kLsThreads < W; w += 4 * kLsThreads) {  // four loads in flight per thread
+    const u64 a = row[w], b = row[w + kLsThreads], d = row[w + 2 * kLsThreads], f = row[w + 3 * kLsThreads];
+    c += (uint32_t)(__popcll(a) + __popcll(b) + __popcll(d) + __popcll(f));
+  }
+  for (; w < W; w += kLsThreads) c += (uint32_t)__popcll(row[w]);
+  const uint32_t t = block_sum<uint32_t>(c, red);
+  if (threadIdx.x == 0) loads[(int64_t)l * E + e] = t;
+}
+
+template <typename T>
+__device__ __forceinline__ double prob(const T* p, int64_t idx);
+template <>
+__device__ __forceinline__ double prob<float>(const float* p, int64_t idx) {
+  return (double)p[idx];
+}
+template <>
+__device__ __forceinline__ double prob<uint16_t>(const uint16_t* p, int64_t idx) {
+  return (double)__uint_as_float((uint32_t)p[idx] << 16);
+}
+
+// blockIdx.x = token slice, blockIdx.y = layer.  Each thread sums the
+// probabilities of fixed columns over the slice's rows, then the block adds
+// sum_i n_i * (its column sums) into out[layer].lbl.  E <= 256: thread tid
+// takes column tid % E and rows tid / E, tid / E + E', ... with E' = 256 / E
+// rows per step (threads past E' * E idle); E > 256: columns tid, tid + 256, ...
+template <typename T>
+__global__ __launch_bounds__(kLsThreads) void k_lbl_sums(const T* p, int64_t N, int32_t E, int64_t rows_per_block,
+                                                         const uint32_t* loads, do_load_stats_result* out) {
+  __shared__ double red[kLsThreads / kWave];
+  const int l = blockIdx.y;
+  const int64_t t0 = (int64_t)blockIdx.x * rows_per_block;
+  const int64_t t1 = min(N, t0 + rows_per_block);
+  const T* pl = p + (int64_t)l * N * E;
+  const uint32_t* nl = loads + (int64_t)l * E;
+  double acc = 0.0;
+  if (E <= kLsThreads) {
+    const int rs = kLsThreads / E;  // rows per step
+    const int col = threadIdx.x % E, r0 = threadIdx.x / E;
+    if (r0 < rs) {
+      double s[kLsUnroll];  // independent sums: kLsUnroll loads in flight per thread
+#pragma unroll
+      for (int u = 0; u < kLsUnroll; ++u) s[u] = 0.0;
+      int64_t t = t0 + r0;
+      for (; t + (kLsUnroll - 1) * rs < t1; t += kLsUnroll * rs) {
+#pragma unroll
+        for (int u = 0; u < kLsUnroll; ++u) s[u] += prob<T>(pl, (t + u * rs) * E + col);
+      }
+      for (; t < t1; t += rs) s[0] += prob<T>(pl, t * E + col);
+      double tsum = 0.0;
+#pragma unroll
+      for (int u = 0; u < kLsUnroll; ++u) tsum += s[u];
+      acc = (double)nl[col] * tsum;
+    }
+  } else {
+    for (int col = threadIdx.x; col < E; col += kLsThreads) {
+      double s = 0.0;
+      for (int64_t t = t0; t < t1; ++t) s += prob<T>(pl, t * E + col);
+      acc += (double)nl[col] * s;
+    }
+  }
+  const double b = block_sum<double>(acc, red);
+  if (threadIdx.x == 0 && b != 0.0) atomicAdd(&out[l].lbl, b);
+}
+
+// One block per layer: total / max / min of the loads, MaxVio over the rank
+// placement, and the Local-LBL scaling.  out[l].lbl holds the raw sum (or 0).
+__global__ __launch_bounds__(kLsThreads) void k_load_finalize(const uint32_t* loads, int64_t N, int32_t E, int32_t k,
+                                                              const RankMap rm, do_load_stats_result* out) {
+  __shared__ uint64_t rank_load[kMaxE];
+  __shared__ uint64_t red64[kLsThreads / kWave];
+  __shared__ uint32_t redmx[kLsThreads / kWave], redmn[kLsThreads / kWave];
+  __shared__ double redv[kLsThreads / kWave];
+  const int l = blockIdx.x;
+  const uint32_t* nl = loads + (int64_t)l * E;
+  const int R = rm.given ? rm.R : E;
+  for (int r = threadIdx.x; r < R; r += kLsThreads) rank_load[r] = 0;
+  __syncthreads();
+  uint64_t tot = 0;
+  uint32_t mx = 0, mn = 0xFFFFFFFFu;
+  for (int i = threadIdx.x; i < E; i += kLsThreads) {
+    const uint32_t n = nl[i];
+    tot += n;
+    mx = max(mx, n);
+    mn = min(mn, n);
+    atomicAdd(reinterpret_cast<unsigned long long*>(&rank_load[rm.given ? rm.rank[i] : i]), (unsigned long long)n);
+  }
+  const uint64_t T = block_sum<uint64_t>(tot, red64);
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    mx = max(mx, (uint32_t)__shfl_xor((int)mx, d));
+    mn = min(mn, (uint32_t)__shfl_xor((int)mn, d));
+  }
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  if (lane == 0) {
+    redmx[w] = mx;
+    redmn[w] = mn;
+  }
+  __syncthreads();  // also orders the rank-load atomics before the reads below
+  __shared__ uint64_t total_s;
+  if (threadIdx.x == 0) total_s = T;
+  __syncthreads();
+  // tau = total / R; |L_r / tau - 1| = |R L_r - total| / total, exact in integers up to the division
+  const uint64_t tot_all = total_s;
+  double v = 0.0;
+  if (tot_all > 0)
+    for (int r = threadIdx.x; r < R; r += kLsThreads) {
+      const uint64_t a = (uint64_t)R * rank_load[r];
+      const uint64_t dev = a > tot_all ? a - tot_all : tot_all - a;
+      v = max(v, (double)dev / (double)tot_all);
+    }
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) v = max(v, __shfl_xor(v, d));
+  if (lane == 0) redv[w] = v;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t M = 0, m = 0xFFFFFFFFu;
+    double V = 0.0;
+    for (int i = 0; i < (int)(blockDim.x >> 6); ++i) {
+      M = max(M, redmx[i]);
+      m = min(m, redmn[i]);
+      V = max(V, redv[i]);
+    }
+    do_load_stats_result& o = out[l];
+    o.total = tot_all;
+    o.max_load = M;
+    o.min_load = m;
+    o.maxvio = V;
+    o.lbl = o.lbl / ((double)N * (double)N * (double)k);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_load_stats(const u64* bits, int64_t N, int64_t ld, int32_t E, int32_t k, int32_t L, const void* p,
+                             do_dtype dt, const RankMap& rm, uint32_t* loads, do_load_stats_result* out,
+                             hipStream_t s) {
+  const int64_t W = (N + 63) / 64;
+  hipError_t e = launch_fill_u64(reinterpret_cast<u64*>(out), (int64_t)L * (sizeof(do_load_stats_result) / 8), s);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_row_loads, dim3((unsigned)E, (unsigned)L), dim3(kLsThreads), 0, s, bits, W, ld, E, loads);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (p != nullptr) {
+    // about 8 blocks per CU in total, each over a contiguous slice of rows
+    const DevInfo di = device_info();
+    const int64_t want = std::max<int64_t>(1, (int64_t)di.cu_count * 8 / L);
+    const int64_t rows = std::max<int64_t>(1, (N + want - 1) / want);
+    const int64_t slices = (N + rows - 1) / rows;
+    if (dt == DO_F32)
+      hipLaunchKernelGGL(k_lbl_sums<float>, dim3((unsigned)slices, (unsigned)L), dim3(kLsThreads), 0, s,
+                         static_cast<const float*>(p), N, E, rows, loads, out);
+    else
+      hipLaunchKernelGGL(k_lbl_sums<uint16_t>, dim3((unsigned)slices, (unsigned)L), dim3(kLsThreads), 0, s,
+                         static_cast<const uint16_t*>(p), N, E, rows, loads, out);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(k_load_finalize, dim3((unsigned)L), dim3(kLsThreads), 0, s, loads, N, E, k, rm, out);
+  return hipGetLastError();
+}
+
+}  // namespace dol

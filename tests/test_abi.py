@@ -30,7 +30,8 @@ def _declared():
 def test_header_declares_the_path(dl):
     names = _declared()
     for must in ("do_topk_signature", "do_pairwise_hamming", "do_loss", "do_fused", "do_stream_create",
-                 "do_stream_append", "do_stream_append_many", "do_stream_finalize", "do_surrogate"):
+                 "do_stream_append", "do_stream_append_many", "do_stream_finalize", "do_surrogate",
+                 "do_load_stats"):
         assert must in names
 
 
@@ -112,6 +113,35 @@ def test_hamming_and_loss_reject(dl):
 ])
 def test_surrogate_rejects(dl, args, expect):
     assert _st(dl, "do_surrogate", *args) == expect
+    assert dl.lib().do_last_error()
+
+
+def _ranks(vals):
+    return (ctypes.c_int32 * len(vals))(*vals)
+
+
+@pytest.mark.parametrize("args,expect", [
+    ((None, 64, 0, 8, 2, 1, None, 0, None, 0, FAKE, FAKE, None), 1),            # NULL bits
+    ((FAKE + 4, 64, 0, 8, 2, 1, None, 0, None, 0, FAKE, FAKE, None), 1),        # misaligned bits
+    ((FAKE, 64, 0, 8, 2, 1, None, 0, None, 0, None, FAKE, None), 1),            # NULL loads
+    ((FAKE, 64, 0, 8, 2, 1, None, 0, None, 0, FAKE, None, None), 1),            # NULL out
+    ((FAKE, 64, 0, 8, 2, 1, None, 0, None, 0, FAKE, FAKE + 4, None), 1),        # out not 8-byte aligned
+    ((FAKE, 130, 2, 8, 2, 1, None, 0, None, 0, FAKE, FAKE, None), 1),           # ld < ceil(N/64)
+    ((FAKE, 64, 0, 8, 9, 1, None, 0, None, 0, FAKE, FAKE, None), 1),            # k > E
+    ((FAKE, 64, 0, 8, 2, 1, FAKE, 7, None, 0, FAKE, FAKE, None), 2),            # bad dtype with p
+    ((FAKE, 64, 0, 8, 2, 1, FAKE + 2, 0, None, 0, FAKE, FAKE, None), 1),        # fp32 p misaligned
+    ((FAKE, 64, 0, 4, 2, 1, None, 0, "bad_rank", 2, FAKE, FAKE, None), 1),      # a rank >= R
+    ((FAKE, 64, 0, 4, 2, 1, None, 0, "ok_rank", 0, FAKE, FAKE, None), 1),       # R = 0
+    ((FAKE, 64, 0, 4, 2, 1, None, 0, "ok_rank", 1025, FAKE, FAKE, None), 1),    # R > 1024
+    ((FAKE, 1 << 32, 0, 8, 2, 1, None, 0, None, 0, FAKE, FAKE, None), 4),       # N >= 2^32
+])
+def test_load_stats_rejects(dl, args, expect):
+    args = list(args)
+    if args[8] == "bad_rank":
+        args[8] = _ranks([0, 1, 2, 1])
+    elif args[8] == "ok_rank":
+        args[8] = _ranks([0, 0, 0, 0])
+    assert _st(dl, "do_load_stats", *args) == expect
     assert dl.lib().do_last_error()
 
 
