@@ -228,6 +228,25 @@ def bench_layers(args, cfg):
     s_ms = sum(a.elapsed_time(b) for a, b in sv) / len(sv)
     s_bytes = tokens * (2 * E * 4 + E // 8) if w["dtype"] == 0 else tokens * (E * 2 + E * 4 + E // 8)
     del sgrad
+    # load statistics (loads, Local-LBL with the scores as probabilities, MaxVio
+    # over 8 ranks of E/8 consecutive experts) on the same signatures
+    ranks = [i * 8 // E for i in range(E)]
+    ls_loads, ls_out = dl.do_load_stats(bits, N, k, p=scores, expert_rank=ranks, R=8)
+    torch.cuda.synchronize()
+    lv = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    for a, b in lv:
+        a.record()
+        b.record()
+    torch.cuda.synchronize()
+    for a, b in lv:
+        a.record()
+        dl.do_load_stats(bits, N, k, p=scores, expert_rank=ranks, R=8, loads=ls_loads, out=ls_out)
+        b.record()
+    torch.cuda.synchronize()
+    ls_ms = sum(a.elapsed_time(b) for a, b in lv) / len(lv)
+    ls_bytes = tokens * (E * elem + E // 8)
+    ls_rec = dl.load_stats_records(ls_out)[0]
+    assert ls_rec["total"] == N * k
     res = dict(
         metric="DO-loss tokens/s per layer (top-k→signature→E×E Hamming→loss); % of HBM peak",
         value=tokens / (ms_per_step / 1e3),
@@ -253,6 +272,12 @@ def bench_layers(args, cfg):
                        bytes_per_token=s_bytes // tokens, achieved_gbs=s_bytes / (s_ms / 1e3) / 1e9,
                        frac=s_bytes / (s_ms / 1e3) / 1e9 / HBM_PEAK_GBS,
                        tokens_per_s=tokens / (s_ms / 1e3)),
+        load_stats=dict(kernels="k_row_loads + k_lbl_sums + k_load_finalize (loads, Local-LBL, MaxVio)",
+                        ms=ls_ms, algorithmic_bytes=ls_bytes, bytes_per_token=ls_bytes // tokens,
+                        achieved_gbs=ls_bytes / (ls_ms / 1e3) / 1e9,
+                        frac=ls_bytes / (ls_ms / 1e3) / 1e9 / HBM_PEAK_GBS,
+                        layer0=dict(lbl=ls_rec["lbl"], maxvio_8_ranks=ls_rec["maxvio"], max_load=ls_rec["max_load"],
+                                    min_load=ls_rec["min_load"])),
         wall_s_timed=wall,
         check=dict(layer0_sum=rec[0]["sum"], expected_sum=2 * N * k * (E - k)),
     )
