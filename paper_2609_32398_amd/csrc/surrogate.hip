@@ -15,9 +15,9 @@
 // with R for the range; lane l owns experts 2l, 2l+1 of the range, so the
 // loads of p and the stores of the gradient are coalesced rows and the reads
 // of G for one selected expert j are a contiguous LDS row.  The selected
-// experts of a token are collected per item into a small LDS list (each
-// expert appends itself to the tokens set in its word), so a token's G rows
-// are read with eight independent LDS loads.
+// experts of a token are collected per item into a small LDS list of row
+// offsets (each expert appends itself to the tokens set in its word), so a
+// token's G rows are read with eight independent LDS loads.
 #include <algorithm>
 
 #include "common.h"
@@ -64,18 +64,21 @@ __device__ __forceinline__ double wave_sum(double v) {
 }
 
 // Per-wave LDS scratch of one item: for each of its 64 tokens the number of
-// selected experts and the first kSurMaxK of their indices (unused entries
-// point at the all-zero row E of the tile).  A token with more selected
-// experts than that is summed from the signature words instead.
+// selected experts and the offsets (in 8-byte units of the G tile) of the rows
+// of the first kSurMaxK of them; unused entries point at the all-zero row E.
+// A token with more selected experts than that is summed from the signature
+// words instead.
 constexpr int kSurMaxK = 8;
+constexpr uint32_t kRowUnits = kRange * 4 / 8;  // one G tile row in 8-byte units
 struct WaveLists {
   uint32_t cnt[64];
-  uint16_t idx[64][kSurMaxK];
+  uint16_t off[64][kSurMaxK];
 };
 
 // FULL: the range has 128 experts and E is even (every lane owns two valid,
 // pair-aligned experts), the common case; otherwise lanes and pairs are guarded.
-template <typename T, bool FULL>
+// GRAD: the gradient is written (else only the loss is accumulated).
+template <typename T, bool FULL, bool GRAD>
 __device__ __forceinline__ void surrogate_item(const SurrogateArgs& a, const uint32_t* gt, WaveLists& wl, int E,
                                                int ng, int iw, int r, int layer, int64_t w, int32_t R0, int32_t R1,
                                                double& lacc, int lane) {
@@ -89,13 +92,13 @@ __device__ __forceinline__ void surrogate_item(const SurrogateArgs& a, const uin
   u64 wg[4];
 #pragma unroll
   for (int g = 0; g < 4; ++g) wg[g] = (g < ng && g * 64 + lane < E) ? bl[(int64_t)(g * 64 + lane) * W + w] : 0ull;
-  // token lists: expert g*64 + lane appends itself to the list of every token
-  // whose bit is set in its word (order within a list is irrelevant: summed)
+  // token lists: expert g*64 + lane appends its row offset to the list of
+  // every token whose bit is set in its word (order within a list is
+  // irrelevant: summed)
   wl.cnt[lane] = 0u;
   {
-    const u64 z = 0x0001000100010001ull * (u64)E;  // the zero row E
-    *reinterpret_cast<u64*>(&wl.idx[lane][0]) = z;
-    *reinterpret_cast<u64*>(&wl.idx[lane][4]) = z;
+    const uint32_t z = (uint32_t)E * kRowUnits * 0x10001u;  // the zero row E, twice
+    *reinterpret_cast<uint4*>(&wl.off[lane][0]) = uint4{z, z, z, z};
   }
   __builtin_amdgcn_wave_barrier();
 #pragma unroll
@@ -105,7 +108,7 @@ __device__ __forceinline__ void surrogate_item(const SurrogateArgs& a, const uin
       const int q = __builtin_ctzll(bits);
       bits &= bits - 1;
       const uint32_t slot = atomicAdd(&wl.cnt[q], 1u);
-      if (slot < (uint32_t)kSurMaxK) wl.idx[q][slot] = (uint16_t)(g * 64 + lane);
+      if (slot < (uint32_t)kSurMaxK) wl.off[q][slot] = (uint16_t)((uint32_t)(g * 64 + lane) * kRowUnits);
     }
   }
   __builtin_amdgcn_wave_barrier();
@@ -123,16 +126,17 @@ __device__ __forceinline__ void surrogate_item(const SurrogateArgs& a, const uin
   const int nt = (int)min((int64_t)64, a.N - tok0);
   const int64_t row0 = (int64_t)layer * a.N + tok0;  // global row of token 0 of the word
   const T* prow = reinterpret_cast<const T*>(a.p) + row0 * E;
-  float* grow = a.grad != nullptr ? a.grad + row0 * E : nullptr;
-  const uint32_t* gl = gt + il0;
+  float* grow = GRAD ? a.grad + row0 * E : nullptr;
+  const unsigned char* glb = reinterpret_cast<const unsigned char*>(gt + il0);  // this lane's pair in row 0
 
   // token tb: c = f R - sum_{j selected} G_ij for this lane's two experts
-  auto emit = [&](int tb, float pa, float pb, int32_t acc0, int32_t acc1) {
-    const int32_t c0 = (((w0 >> tb) & 1ull) ? R0 : 0) - acc0;
-    const int32_t c1 = (((w1 >> tb) & 1ull) ? R1 : 0) - acc1;
+  // (fsel0 / fsel1: all ones when the expert selected the token, else 0)
+  auto emit = [&](int tb, float pa, float pb, int32_t fsel0, int32_t fsel1, int32_t acc0, int32_t acc1) {
+    const int32_t c0 = (fsel0 & R0) - acc0;
+    const int32_t c1 = (fsel1 & R1) - acc1;
     if (v0) {
       lacc += (double)pa * (double)c0 + (double)pb * (double)c1;
-      if (grow != nullptr) {
+      if (GRAD) {
         float* g = grow + (int64_t)tb * E + i0;
         if (FULL || (v1 && even)) {
           *reinterpret_cast<float2*>(g) = float2{(float)c0 * a.s32, (float)c1 * a.s32};
@@ -156,37 +160,47 @@ __device__ __forceinline__ void surrogate_item(const SurrogateArgs& a, const uin
     }
   };
 
+  // token tb of the word: its G rows summed for this lane's two experts
+  auto token = [&](int tb, float pa, float pb, uint32_t b0, uint32_t b1, int q) __attribute__((always_inline)) {
+    const uint4 la = *reinterpret_cast<const uint4*>(&wl.off[tb][0]);  // same address (and value) in every lane
+    const uint32_t lw[4] = {la.x, la.y, la.z, la.w};
+    uint2 gv[kSurMaxK];
+#pragma unroll
+    for (int rr = 0; rr < kSurMaxK; ++rr) {
+      const uint32_t u = (rr & 1) ? (lw[rr >> 1] >> 16) : (lw[rr >> 1] & 0xFFFFu);
+      gv[rr] = *reinterpret_cast<const uint2*>(glb + 8u * u);
+    }
+    int32_t acc0 = 0, acc1 = 0;
+#pragma unroll
+    for (int rr = 0; rr < kSurMaxK; ++rr) {
+      acc0 += (int32_t)gv[rr].x;
+      acc1 += (int32_t)gv[rr].y;
+    }
+    const int32_t f0 = -(int32_t)((b0 >> q) & 1u), f1 = -(int32_t)((b1 >> q) & 1u);
+    emit(tb, pa, pb, f0, f1, acc0, acc1);
+  };
   if (__ballot(wl.cnt[lane] > (uint32_t)kSurMaxK) == 0ull) {
     for (int q0 = 0; q0 < nt; q0 += 16) {
       // probabilities of 16 tokens, loaded together before this batch's stores
       float xa[16], xb[16];
 #pragma unroll
       for (int q = 0; q < 16; ++q) load_p(q0 + q, xa[q], xb[q]);
+      const uint32_t b0 = (uint32_t)(w0 >> q0), b1 = (uint32_t)(w1 >> q0);  // this batch's selection bits
+      if (q0 + 16 <= nt) {
+        // a whole batch: straight-line code, so the LDS reads of one token
+        // can be issued while earlier tokens are summed and stored
 #pragma unroll
-      for (int q = 0; q < 16; ++q) {
-        const int tb = q0 + q;
-        if (tb < nt) {  // wave-uniform
-          const uint4 lst = *reinterpret_cast<const uint4*>(&wl.idx[tb][0]);  // same address (and value) in every lane
-          const uint32_t lw[4] = {lst.x, lst.y, lst.z, lst.w};
-          uint2 gv[kSurMaxK];
+        for (int q = 0; q < 16; ++q) token(q0 + q, xa[q], xb[q], b0, b1, q);
+      } else {
 #pragma unroll
-          for (int rr = 0; rr < kSurMaxK; ++rr) {
-            const uint32_t j = (lw[rr >> 1] >> (16 * (rr & 1))) & 0xFFFFu;
-            gv[rr] = *reinterpret_cast<const uint2*>(gl + j * kRange);
-          }
-          int32_t acc0 = 0, acc1 = 0;
-#pragma unroll
-          for (int rr = 0; rr < kSurMaxK; ++rr) {
-            acc0 += (int32_t)gv[rr].x;
-            acc1 += (int32_t)gv[rr].y;
-          }
-          emit(tb, xa[q], xb[q], acc0, acc1);
-        }
+        for (int q = 0; q < 16; ++q)
+          if (q0 + q < nt) token(q0 + q, xa[q], xb[q], b0, b1, q);  // wave-uniform
       }
     }
   } else {
     // some token selected more experts than a list holds (signatures not made
     // by a top-k with k <= kSurMaxK): sum over the set bits of every token
+    const uint32_t* gl = gt + il0;
     for (int tb = 0; tb < nt; ++tb) {
       float pa, pb;
       load_p(tb, pa, pb);
@@ -202,7 +216,7 @@ __device__ __forceinline__ void surrogate_item(const SurrogateArgs& a, const uin
           acc1 += (int32_t)v.y;
         }
       }
-      emit(tb, pa, pb, acc0, acc1);
+      emit(tb, pa, pb, -(int32_t)((w0 >> tb) & 1ull), -(int32_t)((w1 >> tb) & 1ull), acc0, acc1);
     }
   }
   __builtin_amdgcn_wave_barrier();  // the lists are rebuilt by the next item
@@ -263,10 +277,17 @@ __global__ __launch_bounds__(kSurThreads) void k_surrogate(const SurrogateArgs a
     const bool full = iw == kRange && (E & 1) == 0;
     for (int64_t it = sb + wave; it < se; it += kSurWaves) {
       const int64_t w = it - (int64_t)lr * W;
-      if (full)
-        surrogate_item<T, true>(a, gt, lists[wave], E, ng, iw, r, layer, w, R0, R1, lacc, lane);
-      else
-        surrogate_item<T, false>(a, gt, lists[wave], E, ng, iw, r, layer, w, R0, R1, lacc, lane);
+      if (a.grad != nullptr) {
+        if (full)
+          surrogate_item<T, true, true>(a, gt, lists[wave], E, ng, iw, r, layer, w, R0, R1, lacc, lane);
+        else
+          surrogate_item<T, false, true>(a, gt, lists[wave], E, ng, iw, r, layer, w, R0, R1, lacc, lane);
+      } else {
+        if (full)
+          surrogate_item<T, true, false>(a, gt, lists[wave], E, ng, iw, r, layer, w, R0, R1, lacc, lane);
+        else
+          surrogate_item<T, false, false>(a, gt, lists[wave], E, ng, iw, r, layer, w, R0, R1, lacc, lane);
+      }
     }
     sb = se;
   }
