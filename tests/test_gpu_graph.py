@@ -1,0 +1,89 @@
+"""The fused pass and the separate calls under HIP-graph capture.
+
+The library launches only kernels on the caller's stream (its buffers are
+cleared with fill kernels, not memsets), so a captured do_fused replays to the
+same bits, distances and loss as an eager call.  Every replay is checked, with
+eager work and synchronisations between the replays.
+"""
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dl():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_32398_amd as p
+
+    p.lib()
+    return p
+
+
+@pytest.mark.parametrize("E,k,N,L,dtype", [(256, 8, 70_000, 3, 0), (128, 8, 100_001, 2, 1), (37, 5, 5_000, 2, 0)])
+def test_fused_pass_replays_from_a_graph(dl, syn, E, k, N, L, dtype):
+    print(f"[case] graph E={E} k={k} N={N} L={L} dtype={dtype}", flush=True)
+    x = np.stack([syn.normal(4000 + 17 * l + E, N, E, dtype) for l in range(L)])
+    xd = to_dev(x)
+    ref_bits, ref_D, ref_out = dl.do_fused(xd, k, want_bits=True)
+    torch.cuda.synchronize()
+    bits = torch.zeros_like(ref_bits)
+    D = torch.zeros_like(ref_D)
+    out = torch.zeros_like(ref_out)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):  # warm the launch path outside the capture
+        dl.do_fused(xd, k, bits=bits, D=D, out=out)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        dl.do_fused(xd, k, bits=bits, D=D, out=out)
+    for rep in range(3):
+        bits.zero_()
+        D.fill_(-1)
+        out.zero_()
+        y = torch.randn(1 << 20, device="cuda").sum()  # unrelated eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(bits, ref_bits), f"replay {rep}: signatures differ"
+        assert torch.equal(D, ref_D), f"replay {rep}: distances differ"
+        assert torch.equal(out, ref_out), f"replay {rep}: loss records differ"
+        del y
+
+
+def test_separate_calls_replay_from_a_graph(dl, syn):
+    E, k, N = 64, 6, 30_000
+    x = syn.normal(77, N, E, 1)
+    xd = to_dev(x)
+    ref_bits = dl.do_topk_signature(xd, k)
+    ref_D = dl.do_pairwise_hamming(ref_bits, N)
+    ref_out = dl.do_loss(ref_D)
+    torch.cuda.synchronize()
+    bits = torch.zeros_like(ref_bits)
+    D = torch.zeros_like(ref_D)
+    out = torch.zeros_like(ref_out)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        dl.do_topk_signature(xd, k, bits=bits)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        dl.do_topk_signature(xd, k, bits=bits)
+        dl.do_pairwise_hamming(bits, N, D=D)
+        dl.do_loss(D, out=out)
+    for rep in range(3):
+        bits.zero_()
+        D.zero_()
+        out.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(bits, ref_bits) and torch.equal(D, ref_D) and torch.equal(out, ref_out), rep
