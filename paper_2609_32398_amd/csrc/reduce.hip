@@ -166,9 +166,15 @@ __device__ void block_sum2(u64& s1, u64& s2) {
   }
 }
 
+constexpr int kFinRows = 8;  // rows a wave reads before it writes (loads in flight per lane)
+
 // One block per layer.  cacc may alias D: the diagonal is read before any
 // write, and every other element is read and written only by the thread that
-// owns its (i < j) pair.
+// owns its (i < j) pair.  Wave w takes rows [8w, 8w + 8), then 8 rows 8 nw
+// further, ...; its lanes walk the columns right of the diagonal.  A lane
+// loads its entries of all 8 rows of a column block before it computes and
+// writes them, so the reads of a wave overlap instead of forming a chain of
+// memory round trips.  The mirrored (column) writes are strided.
 __global__ __launch_bounds__(1024) void k_finalize(const uint32_t* cacc, uint32_t* D, do_loss_result* out, int E) {
   __shared__ uint32_t diag[kMaxE];
   const int64_t EE = (int64_t)E * E;
@@ -176,17 +182,28 @@ __global__ __launch_bounds__(1024) void k_finalize(const uint32_t* cacc, uint32_
   uint32_t* d = D + blockIdx.x * EE;
   for (int i = threadIdx.x; i < E; i += blockDim.x) diag[i] = c[(int64_t)i * E + i];
   __syncthreads();
+  const int nw = (int)(blockDim.x >> 6), w = (int)(threadIdx.x >> 6), lane = (int)(threadIdx.x & 63);
   u64 s1 = 0, s2 = 0;
-  for (int64_t p = threadIdx.x; p < EE; p += blockDim.x) {
-    const int i = (int)(p / E), j = (int)(p % E);
-    if (i < j) {
-      const uint32_t v = diag[i] + diag[j] - 2u * c[p];
-      d[p] = v;
-      d[(int64_t)j * E + i] = v;
-      s1 += 2ull * v;
-      s2 += 2ull * (u64)v * (u64)v;
-    } else if (i == j) {
-      d[p] = 0u;
+  for (int i0 = w * kFinRows; i0 < E; i0 += nw * kFinRows) {
+    if (lane < kFinRows && i0 + lane < E) d[(int64_t)(i0 + lane) * E + i0 + lane] = 0u;
+    for (int j = ((i0 + 1) & ~63) + lane; j - lane < E; j += 64) {
+      uint32_t cv[kFinRows];
+#pragma unroll
+      for (int r = 0; r < kFinRows; ++r) {
+        const int i = i0 + r;
+        cv[r] = (j > i && j < E) ? c[(int64_t)i * E + j] : 0u;
+      }
+#pragma unroll
+      for (int r = 0; r < kFinRows; ++r) {
+        const int i = i0 + r;
+        if (j > i && j < E) {
+          const uint32_t v = diag[i] + diag[j] - 2u * cv[r];
+          d[(int64_t)i * E + j] = v;
+          d[(int64_t)j * E + i] = v;
+          s1 += 2ull * v;
+          s2 += 2ull * (u64)v * (u64)v;
+        }
+      }
     }
   }
   if (out == nullptr) return;
@@ -194,16 +211,25 @@ __global__ __launch_bounds__(1024) void k_finalize(const uint32_t* cacc, uint32_
   if (threadIdx.x == 0) write_result(out + blockIdx.x, s1, s2, E);
 }
 
+// Sums of a stored D (every off-diagonal entry), 8 rows per wave per pass.
 __global__ __launch_bounds__(1024) void k_loss(const uint32_t* D, do_loss_result* out, int E) {
   const int64_t EE = (int64_t)E * E;
   const uint32_t* d = D + blockIdx.x * EE;
+  const int nw = (int)(blockDim.x >> 6), w = (int)(threadIdx.x >> 6), lane = (int)(threadIdx.x & 63);
   u64 s1 = 0, s2 = 0;
-  for (int64_t p = threadIdx.x; p < EE; p += blockDim.x) {
-    const int i = (int)(p / E), j = (int)(p % E);
-    if (i != j) {
-      const u64 v = d[p];
-      s1 += v;
-      s2 += v * v;
+  for (int i0 = w * kFinRows; i0 < E; i0 += nw * kFinRows) {
+    for (int j = lane; j - lane < E; j += 64) {
+      uint32_t dv[kFinRows];
+#pragma unroll
+      for (int r = 0; r < kFinRows; ++r) {
+        const int i = i0 + r;
+        dv[r] = (i < E && j < E && j != i) ? d[(int64_t)i * E + j] : 0u;
+      }
+#pragma unroll
+      for (int r = 0; r < kFinRows; ++r) {
+        s1 += dv[r];
+        s2 += (u64)dv[r] * (u64)dv[r];
+      }
     }
   }
   block_sum2(s1, s2);

@@ -172,10 +172,16 @@ __device__ __forceinline__ void rank_chunk(const unsigned char* sbuf, int lane, 
       insert8<!Traits<T>::kExact>(top, key_f32<GEN>(x.w, e0 + 3, vmask), rej);
     }
   } else {
+    // all eight reads issued up front: their latency overlaps the ranking of
+    // the earlier pieces instead of stalling the wave every two pieces
+    v4u xs[8];
+#pragma unroll
+    for (int v = 0; v < 8; ++v) xs[v] = piece(v);
+    __builtin_amdgcn_sched_barrier(0);  // keep the reads ahead of the ranking
 #pragma unroll
     for (int v = 0; v < 8; ++v) {
       int g[8];
-      const v4u x = piece(v);
+      const v4u x = xs[v];
       const int e0 = (cv0 + v) * 8;
       key_bf16x2<GEN>(x.x, e0 + 0, vmask, g[0], g[1]);
       key_bf16x2<GEN>(x.y, e0 + 2, vmask, g[2], g[3]);
