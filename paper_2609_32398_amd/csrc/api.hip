@@ -119,8 +119,9 @@ struct do_stream_s {
   int64_t capacity;
   int64_t W;
   int64_t tokens;
-  u64* hist;
-  uint32_t* cacc;
+  u64* hist;        // [E][W], at the start of one allocation
+  uint32_t* cacc;   // [E][E], right after the history in the same allocation
+  int64_t words;    // u64 words of the allocation (history + counters, rounded up)
   int device;
 };
 
@@ -272,15 +273,17 @@ DOLOSS_API do_status do_stream_create(int32_t E, int32_t k, int64_t capacity_tok
   h->capacity = capacity_tokens;
   h->W = (capacity_tokens + 63) / 64;
   h->tokens = 0;
+  // one allocation, so that a reset is one fill: the history, then the counters
+  h->words = (int64_t)E * h->W + ((int64_t)E * E + 1) / 2;
   hipError_t e = hipGetDevice(&h->device);
-  if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&h->hist), (size_t)E * h->W * sizeof(u64));
-  if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&h->cacc), (size_t)E * E * sizeof(uint32_t));
-  if (e == hipSuccess) e = hipMemset(h->hist, 0, (size_t)E * h->W * sizeof(u64));
-  if (e == hipSuccess) e = hipMemset(h->cacc, 0, (size_t)E * E * sizeof(uint32_t));
+  if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&h->hist), (size_t)h->words * sizeof(u64));
+  if (e == hipSuccess) {
+    h->cacc = reinterpret_cast<uint32_t*>(h->hist + (int64_t)E * h->W);
+    e = hipMemset(h->hist, 0, (size_t)h->words * sizeof(u64));
+  }
   if (e == hipSuccess) e = hipDeviceSynchronize();
   if (e != hipSuccess) {
     if (h->hist) (void)hipFree(h->hist);
-    if (h->cacc) (void)hipFree(h->cacc);
     delete h;
     return hip_status(e, "do_stream_create");
   }
@@ -361,8 +364,7 @@ DOLOSS_API do_status do_stream_finalize(do_stream* h, uint32_t* D, do_loss_resul
 
 DOLOSS_API do_status do_stream_reset(do_stream* h, hipStream_t stream) {
   DO_TRY(check_handle(h));
-  DO_TRY(hip_status(dol::launch_fill_u64(h->hist, (int64_t)h->E * h->W, stream), "reset"));
-  DO_TRY(hip_status(dol::launch_fill_u32(h->cacc, (int64_t)h->E * h->E, 0u, stream), "reset"));
+  DO_TRY(hip_status(dol::launch_fill_u64(h->hist, h->words, stream), "reset"));  // history and counters
   h->tokens = 0;
   return DO_OK;
 }
@@ -370,11 +372,9 @@ DOLOSS_API do_status do_stream_reset(do_stream* h, hipStream_t stream) {
 DOLOSS_API do_status do_stream_destroy(do_stream* h) {
   if (h == nullptr) return DO_OK;
   hipError_t e = hipDeviceSynchronize();
-  const hipError_t e1 = hipFree(h->hist);
-  const hipError_t e2 = hipFree(h->cacc);
+  const hipError_t e1 = hipFree(h->hist);  // the counters share this allocation
   delete h;
   if (e == hipSuccess) e = e1;
-  if (e == hipSuccess) e = e2;
   return hip_status(e, "do_stream_destroy");
 }
 

@@ -24,9 +24,17 @@ __global__ void k_fill_u32(uint32_t* p, int64_t n, uint32_t v) {
     p[i] = v;
 }
 
+// Zeroes n words; 16-byte stores when p is 16-byte aligned.
 __global__ void k_fill_u64(u64* p, int64_t n) {
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
-    p[i] = 0ull;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if ((reinterpret_cast<uintptr_t>(p) & 15) == 0) {
+    ulonglong2* q = reinterpret_cast<ulonglong2*>(p);
+    for (int64_t i = i0; i < (n >> 1); i += stride) q[i] = make_ulonglong2(0ull, 0ull);
+    if (i0 == 0 && (n & 1)) p[n - 1] = 0ull;
+  } else {
+    for (int64_t i = i0; i < n; i += stride) p[i] = 0ull;
+  }
 }
 
 // grid = (word-chunk blocks, micro-tile slices, layers).  Each thread owns up
@@ -261,7 +269,7 @@ hipError_t launch_fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s) {
 
 hipError_t launch_fill_u64(u64* p, int64_t n, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  const int64_t blocks = std::min<int64_t>((n + 255) / 256, 4096);
+  const int64_t blocks = std::min<int64_t>((n / 2 + 255) / 256 + 1, 4096);
   hipLaunchKernelGGL(k_fill_u64, dim3((unsigned)blocks), dim3(256), 0, s, p, n);
   return hipGetLastError();
 }
