@@ -196,7 +196,9 @@ do_status do_stream_append_many(do_stream* h, const void* const* scores, do_dtyp
                                 int32_t count, hipStream_t stream);
 
 /* Writes the distances D [E][E] and the loss `out` [1] (both device) of all
- * tokens appended so far.  The handle is not modified. */
+ * tokens appended so far.  The history and the counts are not modified.  Calls
+ * on one handle must not overlap in time (use one stream, or synchronise):
+ * the finalize keeps its partial sums in the handle between its blocks. */
 do_status do_stream_finalize(do_stream* h, uint32_t* D, do_loss_result* out, hipStream_t stream);
 
 /* Clears the history and the counters (enqueued on `stream`). */

@@ -121,7 +121,8 @@ struct do_stream_s {
   int64_t tokens;
   u64* hist;        // [E][W], at the start of one allocation
   uint32_t* cacc;   // [E][E], right after the history in the same allocation
-  int64_t words;    // u64 words of the allocation (history + counters, rounded up)
+  u64* fin;         // 3 words after the counters: the split finalize's sums and ticket
+  int64_t words;    // u64 words of the allocation (history, counters, finalize words)
   int device;
 };
 
@@ -274,11 +275,12 @@ DOLOSS_API do_status do_stream_create(int32_t E, int32_t k, int64_t capacity_tok
   h->W = (capacity_tokens + 63) / 64;
   h->tokens = 0;
   // one allocation, so that a reset is one fill: the history, then the counters
-  h->words = (int64_t)E * h->W + ((int64_t)E * E + 1) / 2;
+  h->words = (int64_t)E * h->W + ((int64_t)E * E + 1) / 2 + 3;
   hipError_t e = hipGetDevice(&h->device);
   if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&h->hist), (size_t)h->words * sizeof(u64));
   if (e == hipSuccess) {
     h->cacc = reinterpret_cast<uint32_t*>(h->hist + (int64_t)E * h->W);
+    h->fin = h->hist + (int64_t)E * h->W + ((int64_t)E * E + 1) / 2;
     e = hipMemset(h->hist, 0, (size_t)h->words * sizeof(u64));
   }
   if (e == hipSuccess) e = hipDeviceSynchronize();
@@ -356,7 +358,8 @@ DOLOSS_API do_status do_stream_finalize(do_stream* h, uint32_t* D, do_loss_resul
   DO_TRY(check_handle(h));
   if (D == nullptr || !aligned(D, 4)) return fail(DO_ERR_INVALID_ARG, "D is NULL or not 4-byte aligned");
   if (out == nullptr || !aligned(out, 8)) return fail(DO_ERR_INVALID_ARG, "out is NULL or not 8-byte aligned");
-  if (h->E <= dol::kFastMaxE) return hip_status(dol::launch_finalize(h->cacc, D, out, h->E, 1, stream), "finalize");
+  if (h->E <= dol::kFastMaxE)
+    return hip_status(dol::launch_finalize_split(h->cacc, D, out, h->E, h->fin, stream), "finalize");
   DO_TRY(hip_status(dol::launch_fill_u32(D, (int64_t)h->E * h->E, 0u, stream), "fill"));
   DO_TRY(hip_status(dol::launch_gram_bits(h->hist, h->W, h->E, 1, D, stream), "gram"));
   return hip_status(dol::launch_finalize(D, D, out, h->E, 1, stream), "finalize");

@@ -106,6 +106,10 @@ hipError_t launch_load_stats(const u64* bits, int64_t N, int64_t ld, int32_t E, 
                              hipStream_t s);
 
 // Loss of arbitrary distance matrices.
+// One layer (E <= 256) over ceil(E/8) blocks; fin: three u64 that are zero
+// before the call and zero again after it (cacc must not alias D).
+hipError_t launch_finalize_split(const uint32_t* cacc, uint32_t* D, do_loss_result* out, int32_t E, u64* fin,
+                                 hipStream_t s);
 hipError_t launch_loss(const uint32_t* D, int32_t E, int32_t L, do_loss_result* out, hipStream_t s);
 
 }  // namespace dol

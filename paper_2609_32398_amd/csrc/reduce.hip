@@ -219,6 +219,60 @@ __global__ __launch_bounds__(1024) void k_finalize(const uint32_t* cacc, uint32_
   if (threadIdx.x == 0) write_result(out + blockIdx.x, s1, s2, E);
 }
 
+constexpr int kSplitRows = 8;  // rows per block of the split finalize, one per wave
+
+// The finalize of one layer over ceil(E/8) blocks of 512 threads (E <= 256),
+// for a single layer where one block would leave the GPU idle: wave w of
+// block b owns row 8b + w.  Every block adds its exact (S1, S2) into fin[0],
+// fin[1] and takes a ticket from fin[2]; the block with the last ticket
+// writes the loss record and clears fin for the next call.  All accesses to
+// fin are atomics.  c must not alias D.
+__global__ __launch_bounds__(512) void k_finalize_split(const uint32_t* __restrict__ c, uint32_t* __restrict__ d,
+                                                        do_loss_result* out, int E, u64* fin) {
+  __shared__ uint32_t diag[kFastMaxE];
+  for (int i = threadIdx.x; i < E; i += blockDim.x) diag[i] = c[(int64_t)i * E + i];
+  __syncthreads();
+  const int w = (int)(threadIdx.x >> 6), lane = (int)(threadIdx.x & 63);
+  const int i = (int)blockIdx.x * kSplitRows + w;
+  u64 s1 = 0, s2 = 0;
+  if (i < E) {
+    const int64_t row = (int64_t)i * E;
+    if (lane == 0) d[row + i] = 0u;
+    const uint32_t di = diag[i];
+    uint32_t cv[kFastMaxE / 64];
+#pragma unroll
+    for (int q = 0; q < kFastMaxE / 64; ++q) {
+      const int j = lane + 64 * q;
+      cv[q] = (j > i && j < E) ? c[row + j] : 0u;
+    }
+#pragma unroll
+    for (int q = 0; q < kFastMaxE / 64; ++q) {
+      const int j = lane + 64 * q;
+      if (j > i && j < E) {
+        const uint32_t v = di + diag[j] - 2u * cv[q];
+        d[row + j] = v;
+        d[(int64_t)j * E + i] = v;
+        s1 += 2ull * v;
+        s2 += 2ull * (u64)v * (u64)v;
+      }
+    }
+  }
+  block_sum2(s1, s2);
+  if (threadIdx.x == 0) {
+    atomicAdd(&fin[0], s1);
+    atomicAdd(&fin[1], s2);
+    __threadfence();
+    if (atomicAdd(&fin[2], 1ull) == (u64)gridDim.x - 1) {
+      __threadfence();
+      const u64 S1 = atomicAdd(&fin[0], 0ull), S2 = atomicAdd(&fin[1], 0ull);
+      write_result(out, S1, S2, E);
+      atomicExch(&fin[0], 0ull);
+      atomicExch(&fin[1], 0ull);
+      atomicExch(&fin[2], 0ull);
+    }
+  }
+}
+
 // Sums of a stored D (every off-diagonal entry), 8 rows per wave per pass.
 __global__ __launch_bounds__(1024) void k_loss(const uint32_t* D, do_loss_result* out, int E) {
   const int64_t EE = (int64_t)E * E;
@@ -296,6 +350,14 @@ hipError_t launch_gram_bits(const u64* bits, int64_t W, int32_t E, int32_t L, ui
 hipError_t launch_finalize(const uint32_t* cacc, uint32_t* D, do_loss_result* out, int32_t E, int32_t L,
                            hipStream_t s) {
   hipLaunchKernelGGL(k_finalize, dim3((unsigned)L), dim3(1024), 0, s, cacc, D, out, E);
+  return hipGetLastError();
+}
+
+hipError_t launch_finalize_split(const uint32_t* cacc, uint32_t* D, do_loss_result* out, int32_t E, u64* fin,
+                                 hipStream_t s) {
+  if (E > kFastMaxE) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_finalize_split, dim3((unsigned)((E + kSplitRows - 1) / kSplitRows)), dim3(kSplitRows * kWave), 0,
+                     s, cacc, D, out, E, fin);
   return hipGetLastError();
 }
 

@@ -87,3 +87,44 @@ def test_separate_calls_replay_from_a_graph(dl, syn):
         g.replay()
         torch.cuda.synchronize()
         assert torch.equal(bits, ref_bits) and torch.equal(D, ref_D) and torch.equal(out, ref_out), rep
+
+
+def test_stream_reset_append_finalize_replays_from_a_graph(dl, syn):
+    # the stream finalize keeps its cross-block sums in the handle and clears
+    # them itself: repeated finalize calls and graph replays give one result
+    E, k, n, nmb = 128, 8, 5_000, 4
+    print(f"[case] graph stream E={E} k={k} n={n} x{nmb}", flush=True)
+    mbs = [to_dev(syn.normal(300 + b, n, E, 1)) for b in range(nmb)]
+    s = dl.DoStream(E, k, nmb * n)
+    s.append_many(mbs)
+    ref_D, ref_out = s.finalize()
+    torch.cuda.synchronize()
+    D2, out2 = s.finalize()
+    torch.cuda.synchronize()
+    assert torch.equal(D2, ref_D) and torch.equal(out2, ref_out), "second finalize differs"
+    D = torch.zeros_like(ref_D)
+    out = torch.zeros_like(ref_out)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        s.reset()
+        s.append_many(mbs)
+        s.finalize(D, out)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        s.reset()
+        s.append_many(mbs)
+        s.finalize(D, out)
+    for rep in range(3):
+        D.fill_(-1)
+        out.zero_()
+        y = torch.randn(1 << 20, device="cuda").sum()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(D, ref_D), f"replay {rep}: distances differ"
+        assert torch.equal(out, ref_out), f"replay {rep}: loss records differ"
+        del y
+    s.close()
