@@ -147,10 +147,13 @@ __device__ __forceinline__ void surrogate_item(const SurrogateArgs& a, const uin
       }
     }
   };
+  // Every batch position loads: a token past the word's last one reads the
+  // last token's row instead, and its values are never used.  A branch on
+  // tb < nt would make each load wait for its data before the next one.
   auto load_p = [&](int tb, float& pa, float& pb) {
     pa = pb = 0.f;
-    if (tb < nt && v0) {
-      const int64_t off = (int64_t)tb * E + i0;
+    if (v0) {
+      const int64_t off = (int64_t)min(tb, nt - 1) * E + i0;
       if (FULL || (v1 && even)) {
         Prob<T>::pair(prow, off, pa, pb);
       } else {
