@@ -132,3 +132,41 @@ def test_workload4_full(dl, orc, syn):
             assert np.array_equal(words, ref_bits), f"layer {l}: signatures differ"
             np.testing.assert_array_equal(got_D[l], ref_D, err_msg=f"layer {l}")
             loss_close(recs[l], ref_L)
+
+
+def test_more_than_2_31_tokens(dl, orc):
+    # token indices, signature words and sums past 32 bits: E = 2, k = 1 and
+    # N = 2^31 + 100 (the largest expert count the overflow check allows at this
+    # N).  Every token selects exactly one of the two experts, so the rows are
+    # complements, D_01 = N and the loss is 2 N^2.  Sampled tokens are compared
+    # with the oracle's Top-K of those rows.
+    N, E, k = (1 << 31) + 100, 2, 1
+    print(f"[case] N={N} E={E} k={k} fp32", flush=True)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(0x32398)
+    x = torch.randn((N, E), dtype=torch.float32, device="cuda", generator=g)
+    x[N - 7] = 0.5  # a tie near the end: the lower index wins
+    bits, D, out = dl.do_fused(x, k, want_bits=True)
+    torch.cuda.synchronize()
+    W = (N + 63) // 64
+    b = bits.view(E, W)
+    full = W - 1
+    assert bool(torch.all((b[0, :full] ^ b[1, :full]) == -1)), "rows are not complements"
+    assert bool(torch.all((b[0] & b[1]) == 0)), "a token selected both experts"
+    tail = (1 << (N % 64)) - 1
+    assert int(b[0, full] ^ b[1, full]) & ((1 << 64) - 1) == tail, "tail word"
+    lut = torch.tensor([bin(i).count("1") for i in range(256)], dtype=torch.int64, device="cuda")
+    n0 = int(lut[b[0].contiguous().view(torch.uint8).long()].sum())
+    assert n0 == int((x[:, 0] >= x[:, 1]).sum()), "load of expert 0"
+    assert D.view(E, E).cpu().numpy().view(np.uint32).astype(np.int64).tolist() == [[0, N], [N, 0]]
+    rec = dl.loss_records(out)[0]
+    assert rec["sum"] == 2 * N and rec["sumsq"] == 2 * N * N
+    assert rec["loss"] == float(2 * N * N) and rec["mean"] == float(N) and rec["var"] == 0.0
+    rng = np.random.default_rng(7)
+    ts = np.unique(np.concatenate([rng.integers(0, N, 2000), [0, 63, 64, (1 << 31) - 1, 1 << 31, N - 7, N - 1]]))
+    rows = x[torch.from_numpy(ts).cuda()].cpu().numpy()
+    F = orc.topk_signature(rows, k)  # [E][len(ts)] booleans of the sampled rows
+    words = b[:, torch.from_numpy(ts // 64).cuda()].cpu().numpy().view(np.uint64)
+    got = ((words >> (ts % 64).astype(np.uint64)) & np.uint64(1)).astype(bool)
+    assert np.array_equal(got, np.asarray(F, dtype=bool)), "sampled tokens differ from the oracle"
+    del x, bits
