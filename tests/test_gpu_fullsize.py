@@ -170,3 +170,27 @@ def test_more_than_2_31_tokens(dl, orc):
     got = ((words >> (ts % 64).astype(np.uint64)) & np.uint64(1)).astype(bool)
     assert np.array_equal(got, np.asarray(F, dtype=bool)), "sampled tokens differ from the oracle"
     del x, bits
+
+
+def test_maximum_layer_count(dl):
+    # L = 65535 layers (1,024 launches of 64 layers; one finalize block per
+    # layer) of one token each, E = 2, k = 1: in every layer the token selects
+    # the expert with the larger score (expert 0 on a tie), so D_01 = 1 and
+    # the loss is 2.
+    L, N, E, k = 65535, 1, 2, 1
+    print(f"[case] L={L} N={N} E={E} k={k} fp32", flush=True)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(65535)
+    x = torch.randn((L, N, E), dtype=torch.float32, device="cuda", generator=g)
+    x[100, 0, :] = -1.25  # a tie
+    bits, D, out = dl.do_fused(x, k, want_bits=True)
+    torch.cuda.synchronize()
+    b = bits.view(L, E).cpu().numpy()
+    want0 = (x[:, 0, 0] >= x[:, 0, 1]).cpu().numpy()
+    assert np.array_equal(b[:, 0], want0.astype(np.int64)), "expert 0 bits"
+    assert np.array_equal(b[:, 1], (~want0).astype(np.int64)), "expert 1 bits"
+    Dn = D.view(L, E, E).cpu().numpy()
+    assert np.all(Dn[:, 0, 1] == 1) and np.all(Dn[:, 1, 0] == 1) and np.all(Dn[:, 0, 0] == 0) and np.all(Dn[:, 1, 1] == 0)
+    recs = dl.loss_records(out)
+    assert len(recs) == L
+    assert all(r["sum"] == 2 and r["sumsq"] == 2 and r["loss"] == 2.0 and r["var"] == 0.0 for r in recs)
