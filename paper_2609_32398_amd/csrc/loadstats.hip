@@ -54,13 +54,14 @@ __global__ __launch_bounds__(kLsThreads) void k_row_loads(const u64* bits, int64
 
 template <typename T>
 __device__ __forceinline__ double prob(const T* p, int64_t idx);
+// read once: non-temporal loads
 template <>
 __device__ __forceinline__ double prob<float>(const float* p, int64_t idx) {
-  return (double)p[idx];
+  return (double)__builtin_nontemporal_load(p + idx);
 }
 template <>
 __device__ __forceinline__ double prob<uint16_t>(const uint16_t* p, int64_t idx) {
-  return (double)__uint_as_float((uint32_t)p[idx] << 16);
+  return (double)__uint_as_float((uint32_t)__builtin_nontemporal_load(p + idx) << 16);
 }
 
 // blockIdx.x = token slice, blockIdx.y = layer.  Each thread sums the
