@@ -382,8 +382,9 @@ def bench_stream(args):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
-              "(the distances are additive over token shards; see the design notes).", file=sys.stderr)
+        print("bench.py runs on exactly one GPU: there is no multi-GPU path. The distances are additive "
+              "over token shards, so N GPUs would each run this pass on their shard and sum the counters "
+              "with one all-reduce; that path is not built.", file=sys.stderr)
         sys.exit(2)
     ensure_built()
     import torch
