@@ -31,7 +31,7 @@
  *                        bits past N are zero
  *     D       [L][E][E]  uint32, symmetric, zero diagonal
  *     out     [L]        do_loss_result
- * - Ranking rule for Top-K (the paper gives none; see the design notes):
+ * - Ranking rule for Top-K (the paper gives none; this is the library's reading):
  *   larger score first; equal scores go to the lower expert index; -0.0 and
  *   +0.0 are equal; NaN ranks below every number (including -inf) and all NaNs
  *   are equal.  Scores are ranked exactly as given: no gating is applied.

@@ -32,7 +32,7 @@
  *                          the MaxVio imbalance of App. E over a placement of
  *                          the experts on ranks.
  *
- * Readings where the paper is silent (each listed in the design notes):
+ * Readings where the paper is silent:
  *   - ties in Top-K go to the lower expert index;
  *   - -0.0 equals +0.0 (IEEE comparison);
  *   - NaN ranks below every number including -inf, and all NaNs tie;
