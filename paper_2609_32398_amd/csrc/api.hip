@@ -165,7 +165,10 @@ DOLOSS_API do_status do_pairwise_hamming(const uint64_t* bits, int64_t N, int32_
   if (D == nullptr || !aligned(D, 4)) return fail(DO_ERR_INVALID_ARG, "D is NULL or not 4-byte aligned");
   const int64_t W = (N + 63) / 64;
   DO_TRY(hip_status(dol::launch_fill_u32(D, (int64_t)L * E * E, 0u, stream), "fill"));
-  DO_TRY(hip_status(dol::launch_gram_bits(reinterpret_cast<const u64*>(bits), W, E, L, D, stream), "gram"));
+  if (E <= dol::kFastMaxE && dol::gram_mfma_enabled())
+    DO_TRY(hip_status(dol::launch_gram_mfma(reinterpret_cast<const u64*>(bits), W, E, L, D, stream), "gram"));
+  else
+    DO_TRY(hip_status(dol::launch_gram_bits(reinterpret_cast<const u64*>(bits), W, E, L, D, stream), "gram"));
   return hip_status(dol::launch_finalize(D, D, nullptr, E, L, stream), "finalize");
 }
 

@@ -1221,6 +1221,79 @@ Sched tuned_schedule(do_dtype dt, const SegTable& tab, const PathArgs& a, bool f
   return kSchedCand[0];
 }
 
+// ---------------------------------------------------------------------------
+// Gram of stored signatures (do_pairwise_hamming, E <= 256) on the same fp4
+// MFMA tiles as k_topk.  Block b takes layer b / bpl and the part b % bpl of
+// that layer's 8-word chunks, kGramGroup chunks per step.  A chunk's words of
+// every expert are staged in LDS in the bit-tile layout of k_topk (word s of
+// expert e at s * EPW + (e ^ bt_swz(s))); the next step's words are loaded
+// into registers while the current step is multiplied, so one barrier and one
+// memory round trip cover kGramGroup chunks.  Each block adds its counts into
+// cacc at the end; its chunk count stays below 2^24 / 512 (exact fp32 counts).
+// ---------------------------------------------------------------------------
+constexpr int64_t kGramMaxChunks = ((1 << 24) / 512) - 1;
+constexpr int kGramGroup = 4;  // chunks per step
+
+template <int EP>
+__global__ __launch_bounds__(kFusedThreads) void k_gram_mfma(const u64* bits, int64_t W, int E, int L, int bpl,
+                                                             uint32_t* cacc, bool pair64) {
+  constexpr int EPW = EP < 32 ? 32 : EP;
+  constexpr int kTileWords = EPW * kFusedWaves;
+  constexpr int kPer = (kTileWords + kFusedThreads - 1) / kFusedThreads;  // words per thread and chunk (1..4)
+  typedef GramShape<EPW> GS;
+  typedef typename Mfma<GS::TS>::Acc Acc;
+  __shared__ __align__(16) u64 bt[2][kGramGroup][kTileWords];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l = (int)blockIdx.x / bpl, part = (int)blockIdx.x % bpl;
+  if (l >= L) return;
+  const int64_t nch = (W + kFusedWaves - 1) / kFusedWaves;
+  const int64_t c0 = part * nch / bpl, c1 = (part + 1) * nch / bpl;
+  if (c0 >= c1) return;
+  const u64* lb = bits + (int64_t)l * E * W;
+  const WaveTiles wt = wave_tiles(GS::T, wave);
+  Acc acc[kGP];
+#pragma unroll
+  for (int p = 0; p < kGP; ++p)
+#pragma unroll
+    for (int r = 0; r < Mfma<GS::TS>::kRegs; ++r) acc[p][r] = 0.0f;
+  // thread tid holds words (e, s) = (idx / 8, idx % 8) for idx = tid + q * 512
+  // of each chunk: eight threads read an expert's 64 contiguous bytes; chunks
+  // at or past c1 read as zero
+  u64 r[kGramGroup][kPer];
+  auto load = [&](int64_t g0) {
+#pragma unroll
+    for (int g = 0; g < kGramGroup; ++g)
+#pragma unroll
+      for (int q = 0; q < kPer; ++q) {
+        const int idx = tid + q * kFusedThreads, e = idx >> 3;
+        const int64_t w = (g0 + g) * kFusedWaves + (idx & 7);
+        r[g][q] = (idx < kTileWords && g0 + g < c1 && e < E && w < W)
+                      ? __builtin_nontemporal_load(lb + (int64_t)e * W + w)
+                      : 0ull;
+      }
+  };
+  load(c0);
+  int buf = 0;
+  for (int64_t g0 = c0; g0 < c1; g0 += kGramGroup) {
+#pragma unroll
+    for (int g = 0; g < kGramGroup; ++g)
+#pragma unroll
+      for (int q = 0; q < kPer; ++q) {
+        const int idx = tid + q * kFusedThreads, e = idx >> 3, sl = idx & 7;
+        if (idx < kTileWords) bt[buf][g][sl * EPW + (e ^ bt_swz(sl))] = r[g][q];
+      }
+    // the tiles are complete; every wave is done with the tiles written two
+    // steps ago (it multiplied those before reaching this barrier)
+    __syncthreads();
+    if (g0 + kGramGroup < c1) load(g0 + kGramGroup);
+    const int ng = (int)min((int64_t)kGramGroup, c1 - g0);
+    for (int g = 0; g < ng; ++g) mfma_slots<GS::TS>(acc, wt, bt[buf][g], EPW, 0, kFusedWaves, lane);
+    buf ^= 1;
+  }
+  mfma_flush<GS::TS>(acc, wt, cacc + (int64_t)l * E * E, E, lane, (int)(blockIdx.x % kGP), pair64);
+}
+
 }  // namespace
 
 hipError_t launch_topk(do_dtype dt, SegTable& tab, int nseg, const PathArgs& a, bool fast_ok, hipStream_t s) {
@@ -1243,6 +1316,33 @@ hipError_t launch_topk(do_dtype dt, SegTable& tab, int nseg, const PathArgs& a, 
   const hipError_t e = dt == DO_F32 ? launch_ep<float>(tab, a, fast, sc, s) : launch_ep<uint16_t>(tab, a, fast, sc, s);
   if (e != hipSuccess || ev[1] == nullptr) return e;
   return hipEventRecord(ev[1], s);
+}
+
+bool gram_mfma_enabled() { return gram_mode() == kGramMfma; }
+
+hipError_t launch_gram_mfma(const u64* bits, int64_t W, int32_t E, int32_t L, uint32_t* cacc, hipStream_t s) {
+  if (E > kFastMaxE || W < 1) return hipErrorInvalidValue;
+  const int64_t nch = (W + kFusedWaves - 1) / kFusedWaves;
+  const DevInfo di = device_info();
+  // about as many blocks as fit on the GPU at once (two per CU up to 128
+  // experts, one at 256 where the kernel takes 208 VGPRs), each below the
+  // exact-count limit; every block flushes its counts with atomics at its end
+  const int64_t per_cu = E <= 128 ? 2 : 1;
+  int64_t bpl = std::max<int64_t>(1, ((int64_t)di.cu_count * per_cu + L - 1) / L);
+  bpl = std::max<int64_t>(bpl, (nch + kGramMaxChunks - 1) / kGramMaxChunks);
+  bpl = std::min<int64_t>(bpl, nch);
+  if ((int64_t)L * bpl > 0x7FFFFFFF) return hipErrorInvalidValue;
+  const bool pair64 = (E & 1) == 0 && (reinterpret_cast<uintptr_t>(cacc) & 7) == 0;
+  const dim3 grid((unsigned)(L * bpl));
+  if (E <= 32)
+    hipLaunchKernelGGL(k_gram_mfma<32>, grid, dim3(kFusedThreads), 0, s, bits, W, E, L, (int)bpl, cacc, pair64);
+  else if (E <= 64)
+    hipLaunchKernelGGL(k_gram_mfma<64>, grid, dim3(kFusedThreads), 0, s, bits, W, E, L, (int)bpl, cacc, pair64);
+  else if (E <= 128)
+    hipLaunchKernelGGL(k_gram_mfma<128>, grid, dim3(kFusedThreads), 0, s, bits, W, E, L, (int)bpl, cacc, pair64);
+  else
+    hipLaunchKernelGGL(k_gram_mfma<256>, grid, dim3(kFusedThreads), 0, s, bits, W, E, L, (int)bpl, cacc, pair64);
+  return hipGetLastError();
 }
 
 }  // namespace dol

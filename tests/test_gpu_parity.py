@@ -317,3 +317,20 @@ def test_stream_wide_E_gram_at_finalize(dl, orc, syn):
     np.testing.assert_array_equal(D_np(D), ref_D)
     loss_close(dl.loss_records(out)[0], ref_L)
     s.close()
+
+
+@pytest.mark.parametrize("E,k,L,N,offset", [(256, 8, 3, 70_001, 0), (37, 5, 2, 5_000, 1), (128, 8, 5, 100_000, 1),
+                                            (2, 1, 4, 64, 0), (64, 6, 1, 1_000_003, 0)])
+def test_pairwise_hamming_of_stored_layers(dl, orc, syn, E, k, L, N, offset):
+    """do_pairwise_hamming over several layers of oracle signatures; with
+    offset 1 the distances are only 4-byte aligned (32-bit count atomics)."""
+    print(f"[case] hamming E={E} k={k} L={L} N={N} offset={offset}", flush=True)
+    Fs = [orc.topk_signature(syn.normal(900 + 7 * E + l, N, E, 1), k) for l in range(L)]
+    words = np.stack([orc.pack(F) for F in Fs])
+    big = torch.empty(L * E * E + offset, dtype=torch.int32, device="cuda")
+    D = big[offset:].view(L, E, E)
+    dl.do_pairwise_hamming(torch.from_numpy(words.view(np.int64)).cuda(), N, D=D)
+    torch.cuda.synchronize()
+    got = D_np(D)
+    for l in range(L):
+        np.testing.assert_array_equal(got[l], orc.hamming(Fs[l]), err_msg=f"layer {l}")
