@@ -1034,14 +1034,14 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
   flush(pend.layer);
 }
 
-int g_gram_mode = -1;  // kGramPopc or kGramMfma; read once from DOLOSS_GRAM ("popc" selects popcount)
-
+// kGramPopc or kGramMfma, read once from DOLOSS_GRAM ("popc" selects popcount);
+// a function-local static, so concurrent first calls are safe
 int gram_mode() {
-  if (g_gram_mode < 0) {
+  static const int mode = [] {
     const char* v = getenv("DOLOSS_GRAM");
-    g_gram_mode = (v != nullptr && v[0] == 'p') ? kGramPopc : kGramMfma;
-  }
-  return g_gram_mode;
+    return (v != nullptr && v[0] == 'p') ? kGramPopc : kGramMfma;
+  }();
+  return mode;
 }
 
 // Unit schedule of the Top-K kernel.  gu < 0: chosen per launch
@@ -1052,19 +1052,17 @@ struct Sched {
   int64_t gu;
   int mode;
 };
-bool g_sched_read = false;
-Sched g_sched{-1, 0};
 Sched schedule() {
-  if (!g_sched_read) {
+  static const Sched sched = [] {  // read once (thread-safe initialisation)
     const char* v = getenv("DOLOSS_SCHED");
-    if (v != nullptr && v[0] == 'c') g_sched = Sched{0, 0};
+    if (v != nullptr && v[0] == 'c') return Sched{0, 0};
     if (v != nullptr && (v[0] == 'i' || v[0] == 'x' || v[0] == 'p')) {
       const int n = atoi(v + 1);
-      g_sched = Sched{n > 0 ? n : 4, v[0] == 'i' ? 0 : v[0] == 'x' ? 1 : 2};
+      return Sched{n > 0 ? n : 4, v[0] == 'i' ? 0 : v[0] == 'x' ? 1 : 2};
     }
-    g_sched_read = true;
-  }
-  return g_sched;
+    return Sched{-1, 0};
+  }();
+  return sched;
 }
 
 template <typename T, int EP, int GM>
