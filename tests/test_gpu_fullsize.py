@@ -159,6 +159,9 @@ def test_more_than_2_31_tokens(dl, orc):
     n0 = int(lut[b[0].contiguous().view(torch.uint8).long()].sum())
     assert n0 == int((x[:, 0] >= x[:, 1]).sum()), "load of expert 0"
     assert D.view(E, E).cpu().numpy().view(np.uint32).astype(np.int64).tolist() == [[0, N], [N, 0]]
+    D2 = dl.do_pairwise_hamming(bits, N)  # the stored-signature Gram over 2^25 words per row
+    torch.cuda.synchronize()
+    assert D2.view(E, E).cpu().numpy().view(np.uint32).astype(np.int64).tolist() == [[0, N], [N, 0]]
     rec = dl.loss_records(out)[0]
     assert rec["sum"] == 2 * N and rec["sumsq"] == 2 * N * N
     assert rec["loss"] == float(2 * N * N) and rec["mean"] == float(N) and rec["var"] == 0.0
