@@ -215,31 +215,34 @@ __device__ __forceinline__ u64 exact_key64(uint32_t bits, int e) {
   return ((u64)exact_key(bits) << 32) | (u64)(0xFFFFFFFFu - (uint32_t)e);
 }
 
-// Exact Top-k (k <= 8) of one row in a single pass: insertion of unique
-// 64-bit keys (value key, then the complemented index) into a sorted list.
-// The row is read 16 elements at a time so that the loads of a batch are in
-// flight together instead of one memory round trip per element.
-template <typename T>
-__device__ void exact_topk8_lane(const T* row, int E, int k, u64* bt, int swz, u64 bit) {
-  u64 lst[8];
+// Exact Top-k (k <= KL) of one row in a single pass: insertion of unique
+// 64-bit keys (value key, then the complemented index) into a sorted list of
+// KL entries.  The row is read 16 elements at a time so that the loads of a
+// batch are in flight together instead of one memory round trip per element.
+template <typename T, int KL>
+__device__ void exact_topk_list_lane(const T* row, int E, int k, u64* bt, int swz, u64 bit) {
+  u64 lst[KL];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) lst[i] = 0ull;  // every real key is > 0
+  for (int i = 0; i < KL; ++i) lst[i] = 0ull;  // every real key is > 0
   for (int e0 = 0; e0 < E; e0 += 16) {
+    // all 16 loads issued unconditionally (positions past E re-read element
+    // E - 1 and are skipped below): a branch per load would make each load
+    // wait for its data before the next one is issued
     uint32_t v[16];
 #pragma unroll
-    for (int j = 0; j < 16; ++j) v[j] = (e0 + j < E) ? elem_bits<T>(row, e0 + j) : 0u;
+    for (int j = 0; j < 16; ++j) v[j] = elem_bits<T>(row, min(e0 + j, E - 1));
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
       if (e0 + j >= E) break;
       const u64 key = exact_key64(v[j], e0 + j);
-      if (key <= lst[7]) continue;
+      if (key <= lst[KL - 1]) continue;
 #pragma unroll
-      for (int i = 7; i > 0; --i) lst[i] = max(lst[i], min(lst[i - 1], key));
+      for (int i = KL - 1; i > 0; --i) lst[i] = max(lst[i], min(lst[i - 1], key));
       lst[0] = max(lst[0], key);
     }
   }
 #pragma unroll
-  for (int i = 0; i < 8; ++i)
+  for (int i = 0; i < KL; ++i)
     if (i < k) atomicOr(&bt[(int)(0xFFFFFFFFu - (uint32_t)(lst[i] & 0xFFFFFFFFull)) ^ swz], bit);
 }
 
@@ -253,7 +256,7 @@ __device__ void exact_topk_passes_lane(const T* row, int E, int k, u64* bt, int 
     for (int e0 = 0; e0 < E; e0 += 16) {
       uint32_t v[16];
 #pragma unroll
-      for (int j = 0; j < 16; ++j) v[j] = (e0 + j < E) ? elem_bits<T>(row, e0 + j) : 0u;
+      for (int j = 0; j < 16; ++j) v[j] = elem_bits<T>(row, min(e0 + j, E - 1));  // unconditional, as above
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
         if (e0 + j >= E) break;
@@ -998,7 +1001,9 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
         if (need_slow) {
           const T* row = reinterpret_cast<const T*>(sv.base) + t * (int64_t)E;
           if (k <= 8)
-            exact_topk8_lane<T>(row, E, k, mybt, bt_swz(wave), 1ull << lane);
+            exact_topk_list_lane<T, 8>(row, E, k, mybt, bt_swz(wave), 1ull << lane);
+          else if (k <= 16)
+            exact_topk_list_lane<T, 16>(row, E, k, mybt, bt_swz(wave), 1ull << lane);
           else
             exact_topk_passes_lane<T>(row, E, k, mybt, bt_swz(wave), 1ull << lane);
         }
