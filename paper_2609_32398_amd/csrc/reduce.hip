@@ -74,11 +74,25 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bits(const u64* __restric
   for (int64_t ch = blockIdx.x; ch < nchunks; ch += gridDim.x) {
     const int64_t w0 = ch * kGramSlots;
     __syncthreads();
-    for (int f = tid; f < E4 * kGramSlots; f += kGramThreads) {
-      const int e = f / kGramSlots, s = f % kGramSlots;
-      u64 v = 0;
-      if (e < E && w0 + s < W) v = lb[(int64_t)e * W + w0 + s];
-      tile[s * E4 + e] = v;
+    // eight loads per thread in flight before their stores (a load followed
+    // by its store per iteration would be one memory round trip each);
+    // out-of-range positions read word 0 and store zero
+    constexpr int kB = 8;
+    const int total = E4 * kGramSlots;
+    for (int f0 = tid; f0 < total; f0 += kB * kGramThreads) {
+      u64 v[kB];
+#pragma unroll
+      for (int b = 0; b < kB; ++b) {
+        const int f = f0 + b * kGramThreads, e = f / kGramSlots, s = f % kGramSlots;
+        const bool in = f < total && e < E && w0 + s < W;
+        v[b] = lb[in ? (int64_t)e * W + w0 + s : 0];
+        v[b] = in ? v[b] : 0ull;
+      }
+#pragma unroll
+      for (int b = 0; b < kB; ++b) {
+        const int f = f0 + b * kGramThreads;
+        if (f < total) tile[(f % kGramSlots) * E4 + f / kGramSlots] = v[b];
+      }
     }
     __syncthreads();
     for (int s = 0; s < kGramSlots; ++s) {
