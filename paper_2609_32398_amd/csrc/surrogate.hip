@@ -269,9 +269,22 @@ __global__ __launch_bounds__(kSurThreads) void k_surrogate(const SurrogateArgs a
     }
     __syncthreads();  // every wave is done with the previous tile
     const uint32_t* Dl = a.D + (int64_t)layer * E * E;
-    for (int idx = tid; idx < E * kRange; idx += kSurThreads) {  // rows i of the range, read along j
-      const int il = idx / E, j = idx - il * E;
-      gt[j * kRange + il] = il < iw ? Dl[(int64_t)(r * kRange + il) * E + j] : 0u;
+    // rows i of the range, read along j, eight loads in flight per thread
+    // before their stores; positions outside read entry 0 and store zero
+    for (int idx0 = tid; idx0 < E * kRange; idx0 += 8 * kSurThreads) {
+      uint32_t v[8];
+#pragma unroll
+      for (int b = 0; b < 8; ++b) {
+        const int idx = idx0 + b * kSurThreads, il = idx / E, j = idx - il * E;
+        const bool in = idx < E * kRange && il < iw;
+        v[b] = Dl[in ? (int64_t)(r * kRange + il) * E + j : 0];
+        v[b] = in ? v[b] : 0u;
+      }
+#pragma unroll
+      for (int b = 0; b < 8; ++b) {
+        const int idx = idx0 + b * kSurThreads, il = idx / E, j = idx - il * E;
+        if (idx < E * kRange) gt[j * kRange + il] = v[b];
+      }
     }
     __syncthreads();
     for (int il = tid; il < iw; il += kSurThreads) {
