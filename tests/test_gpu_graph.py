@@ -89,10 +89,12 @@ def test_separate_calls_replay_from_a_graph(dl, syn):
         assert torch.equal(bits, ref_bits) and torch.equal(D, ref_D) and torch.equal(out, ref_out), rep
 
 
-def test_stream_reset_append_finalize_replays_from_a_graph(dl, syn):
+@pytest.mark.parametrize("E,k", [(128, 8), (300, 8)])
+def test_stream_reset_append_finalize_replays_from_a_graph(dl, syn, E, k):
     # the stream finalize keeps its cross-block sums in the handle and clears
     # them itself: repeated finalize calls and graph replays give one result
-    E, k, n, nmb = 128, 8, 5_000, 4
+    # (E = 300: the history's Gram is taken at finalize by the popcount kernel)
+    n, nmb = 5_000, 4
     print(f"[case] graph stream E={E} k={k} n={n} x{nmb}", flush=True)
     mbs = [to_dev(syn.normal(300 + b, n, E, 1)) for b in range(nmb)]
     s = dl.DoStream(E, k, nmb * n)
