@@ -187,11 +187,13 @@ typedef struct do_stream_s do_stream;
 do_status do_stream_create(int32_t E, int32_t k, int64_t capacity_tokens, do_stream** out);
 
 /* Appends n_tokens >= 0 tokens of scores [n_tokens][E] (device).  Fails with
- * DO_ERR_CAPACITY, leaving the handle unchanged, if the history would overflow. */
+ * DO_ERR_CAPACITY, leaving the handle unchanged, if the history would overflow.
+ * With n_tokens = 0 nothing is read or launched, and scores may be NULL. */
 do_status do_stream_append(do_stream* h, const void* scores, do_dtype dtype, int64_t n_tokens, hipStream_t stream);
 
 /* Appends `count` (1..64) micro-batches of n_tokens_each tokens in one launch.
- * `scores` is a HOST array of `count` device pointers, read during the call. */
+ * `scores` is a HOST array of `count` device pointers, read during the call;
+ * with n_tokens_each = 0 the device pointers may be NULL. */
 do_status do_stream_append_many(do_stream* h, const void* const* scores, do_dtype dtype, int64_t n_tokens_each,
                                 int32_t count, hipStream_t stream);
 

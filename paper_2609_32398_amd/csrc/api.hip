@@ -312,12 +312,12 @@ do_status stream_append(do_stream* h, const void* const* scores, do_dtype dtype,
   DO_TRY(check_dtype(dtype));
   if (n < 0) return fail(DO_ERR_INVALID_ARG, "n_tokens must be >= 0");
   if (count < 1 || count > dol::kMaxSeg) return fail(DO_ERR_INVALID_ARG, "count must be in [1, 64]");
+  if (n == 0) return DO_OK;  // nothing is read: the score pointers may be NULL
   bool fast = true;
   for (int i = 0; i < count; ++i) {
     DO_TRY(check_scores(scores[i], dtype));
     fast = fast && fast_layout(scores[i], dtype, h->E);
   }
-  if (n == 0) return DO_OK;
   if ((h->capacity - h->tokens) / count < n)
     return fail(DO_ERR_CAPACITY, "append would exceed the history capacity");
   dol::PathArgs a{};

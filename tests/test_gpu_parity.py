@@ -334,3 +334,23 @@ def test_pairwise_hamming_of_stored_layers(dl, orc, syn, E, k, L, N, offset):
     got = D_np(D)
     for l in range(L):
         np.testing.assert_array_equal(got[l], orc.hamming(Fs[l]), err_msg=f"layer {l}")
+
+
+def test_stream_append_of_zero_tokens_changes_nothing(dl, orc, syn):
+    E, k = 64, 6
+    print(f"[case] stream zero-token appends E={E} k={k}", flush=True)
+    x = syn.normal(4242, 3000, E, 1)
+    xd = to_dev(x)
+    s = dl.DoStream(E, k, 5000)
+    s.append(xd[:0])  # a zero-length view: valid pointer, no tokens
+    assert s.tokens == 0
+    s.append(xd[:1234])
+    s.append(xd[1234:1234])
+    s.append_many([xd[:0], xd[5:5]])
+    s.append(xd[1234:])
+    assert s.tokens == 3000
+    D, out = s.finalize()
+    torch.cuda.synchronize()
+    F = orc.topk_signature(x, k)
+    np.testing.assert_array_equal(D_np(D), orc.hamming(F))
+    s.close()
