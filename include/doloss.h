@@ -183,7 +183,8 @@ do_status do_load_stats(const uint64_t* bits, int64_t N, int64_t ld, int32_t E, 
 typedef struct do_stream_s do_stream;
 
 /* Allocates the history (E x ceil(capacity/64) words) and the counters on the
- * current device and zeroes them (synchronously).  *out receives the handle. */
+ * current device and zeroes them (synchronously).  *out receives the handle,
+ * or NULL on failure (DO_ERR_HIP when a device or host allocation fails). */
 do_status do_stream_create(int32_t E, int32_t k, int64_t capacity_tokens, do_stream** out);
 
 /* Appends n_tokens >= 0 tokens of scores [n_tokens][E] (device).  Fails with
@@ -206,7 +207,8 @@ do_status do_stream_finalize(do_stream* h, uint32_t* D, do_loss_result* out, hip
 /* Clears the history and the counters (enqueued on `stream`). */
 do_status do_stream_reset(do_stream* h, hipStream_t stream);
 
-/* Frees the handle (synchronises the device first).  NULL is accepted. */
+/* Frees the handle after synchronising the device it was created on (the
+ * current device is restored).  NULL is accepted. */
 do_status do_stream_destroy(do_stream* h);
 
 /* Device pointer to the history [E][do_stream_words_per_expert(h)]; bits past

@@ -1,6 +1,7 @@
 // Host side of the C ABI declared in include/doloss.h: argument validation,
 // dispatch to the kernels, and the streaming-history handles.
 #include <cstring>
+#include <new>
 #include <string>
 
 #include "common.h"
@@ -271,7 +272,8 @@ DOLOSS_API do_status do_stream_create(int32_t E, int32_t k, int64_t capacity_tok
   *out = nullptr;
   DO_TRY(check_shape(capacity_tokens, E, 1));
   DO_TRY(check_k(k, E));
-  do_stream* h = new do_stream_s{};
+  do_stream* h = new (std::nothrow) do_stream_s{};  // no exception may cross the C ABI
+  if (h == nullptr) return fail(DO_ERR_HIP, "do_stream_create: host allocation failed");
   h->E = E;
   h->k = k;
   h->capacity = capacity_tokens;
@@ -377,8 +379,14 @@ DOLOSS_API do_status do_stream_reset(do_stream* h, hipStream_t stream) {
 
 DOLOSS_API do_status do_stream_destroy(do_stream* h) {
   if (h == nullptr) return DO_OK;
-  hipError_t e = hipDeviceSynchronize();
+  // wait for the handle's own device (the current one may differ), then free
+  int cur = -1;
+  hipError_t e = hipGetDevice(&cur);
+  const bool other = e == hipSuccess && cur != h->device;
+  if (other) e = hipSetDevice(h->device);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
   const hipError_t e1 = hipFree(h->hist);  // the counters share this allocation
+  if (other) (void)hipSetDevice(cur);
   delete h;
   if (e == hipSuccess) e = e1;
   return hip_status(e, "do_stream_destroy");
