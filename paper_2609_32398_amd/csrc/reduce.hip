@@ -29,8 +29,17 @@ __global__ void k_fill_u64(u64* p, int64_t n) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   const int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if ((reinterpret_cast<uintptr_t>(p) & 15) == 0) {
-    ulonglong2* q = reinterpret_cast<ulonglong2*>(p);
-    for (int64_t i = i0; i < (n >> 1); i += stride) q[i] = make_ulonglong2(0ull, 0ull);
+    // four 16-byte stores per thread and pass, written past the caches
+    typedef unsigned long long v2u __attribute__((ext_vector_type(2)));
+    v2u* q = reinterpret_cast<v2u*>(p);
+    const int64_t nq = n >> 1;
+    const v2u z = {0ull, 0ull};
+    int64_t i = i0;
+    for (; i + 3 * stride < nq; i += 4 * stride) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) __builtin_nontemporal_store(z, q + i + u * stride);
+    }
+    for (; i < nq; i += stride) __builtin_nontemporal_store(z, q + i);
     if (i0 == 0 && (n & 1)) p[n - 1] = 0ull;
   } else {
     for (int64_t i = i0; i < n; i += stride) p[i] = 0ull;
@@ -337,7 +346,7 @@ hipError_t launch_fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s) {
 
 hipError_t launch_fill_u64(u64* p, int64_t n, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  const int64_t blocks = std::min<int64_t>((n / 2 + 255) / 256 + 1, 4096);
+  const int64_t blocks = std::min<int64_t>((n / 2 + 1023) / 1024 + 1, 2048);
   hipLaunchKernelGGL(k_fill_u64, dim3((unsigned)blocks), dim3(256), 0, s, p, n);
   return hipGetLastError();
 }
