@@ -285,6 +285,9 @@ def test_stream_unaligned_appends_equal_one_batch(dl, orc, syn):
     D3, out3 = s.finalize()
     torch.cuda.synchronize()
     assert s.tokens == 0 and int(D3.abs().sum()) == 0
+    # the reset fill covers the whole history (12,099 words here: the four-store
+    # passes, the single-store tail and the odd last word)
+    assert not bits_np(s.history()).any(), "history not cleared by the reset"
     s.close()
 
 
