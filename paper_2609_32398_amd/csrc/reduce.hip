@@ -198,14 +198,18 @@ __device__ void block_sum2(u64& s1, u64& s2) {
 }
 
 constexpr int kFinRows = 8;  // rows a wave reads before it writes (loads in flight per lane)
+constexpr int kFinCols = 2;  // 64-column blocks k_finalize reads together
 
 // One block per layer.  cacc may alias D: the diagonal is read before any
 // write, and every other element is read and written only by the thread that
 // owns its (i < j) pair.  Wave w takes rows [8w, 8w + 8), then 8 rows 8 nw
 // further, ...; its lanes walk the columns right of the diagonal.  A lane
-// loads its entries of all 8 rows of a column block before it computes and
-// writes them, so the reads of a wave overlap instead of forming a chain of
-// memory round trips.  The mirrored (column) writes are strided.
+// loads its entries of all 8 rows in up to 2 column blocks (16 loads) before
+// it computes and writes them, so the reads of a wave overlap instead of
+// forming a chain of memory round trips (the stores may alias the loads, so
+// the compiler cannot move later loads above them).  A position outside the
+// upper triangle loads entry 0 and discards it.  The mirrored (column) writes
+// are strided.
 __global__ __launch_bounds__(1024) void k_finalize(const uint32_t* cacc, uint32_t* D, do_loss_result* out, int E) {
   __shared__ uint32_t diag[kMaxE];
   const int64_t EE = (int64_t)E * E;
@@ -217,22 +221,29 @@ __global__ __launch_bounds__(1024) void k_finalize(const uint32_t* cacc, uint32_
   u64 s1 = 0, s2 = 0;
   for (int i0 = w * kFinRows; i0 < E; i0 += nw * kFinRows) {
     if (lane < kFinRows && i0 + lane < E) d[(int64_t)(i0 + lane) * E + i0 + lane] = 0u;
-    for (int j = ((i0 + 1) & ~63) + lane; j - lane < E; j += 64) {
-      uint32_t cv[kFinRows];
+    for (int jb = ((i0 + 1) & ~63) + lane; jb - lane < E; jb += 64 * kFinCols) {
+      uint32_t cv[kFinCols][kFinRows];
 #pragma unroll
-      for (int r = 0; r < kFinRows; ++r) {
-        const int i = i0 + r;
-        cv[r] = (j > i && j < E) ? c[(int64_t)i * E + j] : 0u;
+      for (int q = 0; q < kFinCols; ++q) {
+#pragma unroll
+        for (int r = 0; r < kFinRows; ++r) {
+          const int i = i0 + r, j = jb + 64 * q;
+          const bool in = j > i && j < E;
+          cv[q][r] = c[in ? (uint32_t)(i * E + j) : 0u];  // E <= 1024: offsets fit 32 bits
+        }
       }
 #pragma unroll
-      for (int r = 0; r < kFinRows; ++r) {
-        const int i = i0 + r;
-        if (j > i && j < E) {
-          const uint32_t v = diag[i] + diag[j] - 2u * cv[r];
-          d[(int64_t)i * E + j] = v;
-          d[(int64_t)j * E + i] = v;
-          s1 += 2ull * v;
-          s2 += 2ull * (u64)v * (u64)v;
+      for (int q = 0; q < kFinCols; ++q) {
+#pragma unroll
+        for (int r = 0; r < kFinRows; ++r) {
+          const int i = i0 + r, j = jb + 64 * q;
+          if (j > i && j < E) {
+            const uint32_t v = diag[i] + diag[j] - 2u * cv[q][r];
+            d[(uint32_t)(i * E + j)] = v;
+            d[(uint32_t)(j * E + i)] = v;
+            s1 += 2ull * v;
+            s2 += 2ull * (u64)v * (u64)v;
+          }
         }
       }
     }
