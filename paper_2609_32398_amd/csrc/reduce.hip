@@ -313,18 +313,29 @@ __global__ __launch_bounds__(1024) void k_loss(const uint32_t* D, do_loss_result
   const uint32_t* d = D + blockIdx.x * EE;
   const int nw = (int)(blockDim.x >> 6), w = (int)(threadIdx.x >> 6), lane = (int)(threadIdx.x & 63);
   u64 s1 = 0, s2 = 0;
+  // as in k_finalize: 16 loads per lane (8 rows x 2 column blocks) per round
+  // trip, 32-bit offsets, positions off the matrix or on the diagonal read
+  // entry 0 and count as zero
   for (int i0 = w * kFinRows; i0 < E; i0 += nw * kFinRows) {
-    for (int j = lane; j - lane < E; j += 64) {
-      uint32_t dv[kFinRows];
+    for (int jb = lane; jb - lane < E; jb += 64 * kFinCols) {
+      uint32_t dv[kFinCols][kFinRows];
 #pragma unroll
-      for (int r = 0; r < kFinRows; ++r) {
-        const int i = i0 + r;
-        dv[r] = (i < E && j < E && j != i) ? d[(int64_t)i * E + j] : 0u;
+      for (int q = 0; q < kFinCols; ++q) {
+#pragma unroll
+        for (int r = 0; r < kFinRows; ++r) {
+          const int i = i0 + r, j = jb + 64 * q;
+          const bool in = i < E && j < E && j != i;
+          const uint32_t v = d[in ? (uint32_t)(i * E + j) : 0u];
+          dv[q][r] = in ? v : 0u;
+        }
       }
 #pragma unroll
-      for (int r = 0; r < kFinRows; ++r) {
-        s1 += dv[r];
-        s2 += (u64)dv[r] * (u64)dv[r];
+      for (int q = 0; q < kFinCols; ++q) {
+#pragma unroll
+        for (int r = 0; r < kFinRows; ++r) {
+          s1 += dv[q][r];
+          s2 += (u64)dv[q][r] * (u64)dv[q][r];
+        }
       }
     }
   }
