@@ -222,6 +222,15 @@ def test_loss_of_arbitrary_matrices(dl):
                 assert recs[l]["var"] == pytest.approx((s2 * P - s1 * s1) / (P * P), rel=1e-9)
             else:
                 assert recs[l] == dict(sum=0, sumsq=0, loss=0.0, mean=0.0, var=0.0)
+    # one column past a 128-column load batch, and the largest E: exact sums in
+    # uint64 (entries < 2^20, so the sum of squares stays below 2^60)
+    for E in (129, 1024):
+        D = rng.integers(0, 1 << 20, size=(1, E, E), dtype=np.uint32)
+        out = dl.do_loss(torch.from_numpy(D.view(np.int32)).cuda())
+        torch.cuda.synchronize()
+        rec = dl.loss_records(out)[0]
+        v = D[0][~np.eye(E, dtype=bool)].astype(np.uint64)
+        assert rec["sum"] == int(v.sum()) and rec["sumsq"] == int((v * v).sum()), f"E={E}"
 
 
 def test_hamming_of_oracle_signatures(dl, orc, syn):
