@@ -66,8 +66,10 @@ typedef enum { DO_F32 = 0, DO_BF16 = 1 } do_dtype;
 /* Per-layer result of the loss (device memory, 40 bytes). */
 typedef struct {
   uint64_t sum;   /* exact sum over i != j of D_ij (Eq. 2: equals 2*N*k*(E-k)) */
-  uint64_t sumsq; /* exact sum over i != j of D_ij^2 (Eq. 3) */
-  double loss;    /* Eq. 3 as fp64: L_origin_DO = sum_{i != j} ||F_i - F_j||_1^2 */
+  uint64_t sumsq; /* exact sum over i != j of D_ij^2 (Eq. 3); do_loss saturates it at
+                     2^64 - 1 when the sum does not fit (never for distances of signatures) */
+  double loss;    /* Eq. 3 as fp64: L_origin_DO = sum_{i != j} ||F_i - F_j||_1^2 (the
+                     exact integer sum, rounded; within 2 ulp when sumsq saturates) */
   double mean;    /* sum / (E*(E-1)) */
   double var;     /* population variance of the E*(E-1) off-diagonal D_ij (App. C.1) */
 } do_loss_result;
@@ -95,7 +97,10 @@ do_status do_pairwise_hamming(const uint64_t* bits, int64_t N, int32_t E, int32_
 /*
  * Step 4 (Sec. 3.1.1, Eq. 3; App. C.1): loss and off-diagonal statistics of
  * any E x E distance matrices (the diagonal is ignored; symmetry is not
- * assumed).  For E = 1 every field is zero.
+ * assumed).  For E = 1 every field is zero.  Any uint32 entries are accepted:
+ * the sums are accumulated exactly (the sum of squares in 128 bits, so it
+ * never wraps); `sum` is exact, `sumsq` is exact below 2^64 and saturated at
+ * 2^64 - 1 above, and loss, mean and var are the exact sums rounded to fp64.
  *   D    [L][E][E] device
  *   out  [L] device
  */
@@ -107,7 +112,8 @@ do_status do_loss(const uint32_t* D, int32_t E, int32_t L, do_loss_result* out, 
  * accumulated in `D` itself, which is then turned into distances and reduced
  * to the loss.  Results are identical to do_topk_signature +
  * do_pairwise_hamming + do_loss.
- *   bits  nullable, [L][E][ceil(N/64)] device
+ *   bits  [L][E][ceil(N/64)] device; may be NULL only for E <= 256 (wider E
+ *         re-reads the stored signatures for the Gram: DO_ERR_INVALID_ARG)
  *   D     [L][E][E] device, fully overwritten
  *   out   [L] device
  */
@@ -225,6 +231,22 @@ int64_t do_stream_words_per_expert(const do_stream* h);
  * cancel.  Lets a caller time that kernel alone with hipEventElapsedTime.
  */
 do_status do_profile_next(hipEvent_t start, hipEvent_t stop);
+
+/*
+ * Process-wide overrides of internal choices that never change any result,
+ * for tests and benchmarks (they take effect at the next call; calls already
+ * enqueued are unaffected).  Returns DO_ERR_INVALID_ARG for an unknown option
+ * or a value out of range.
+ *   DO_OPT_SCHEDULE  unit schedule of the score pass: -1 (default) measures
+ *                    both candidates on the first launches of every shape of
+ *                    at least 4 Mi tokens and keeps the faster; 0 fixes the
+ *                    XCD-partitioned schedule; 1 fixes one contiguous range
+ *                    of work units per block.
+ *   DO_OPT_GRAM      co-occurrence Gram for E <= 256: 0 (default) the fp4
+ *                    MFMA Gram, 1 the VALU popcount Gram.
+ */
+typedef enum { DO_OPT_SCHEDULE = 0, DO_OPT_GRAM = 1 } do_option;
+do_status do_set_option(do_option opt, int32_t value);
 
 /* Text of a status code, and the message of the calling thread's last error. */
 const char* do_status_string(do_status s);

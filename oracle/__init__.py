@@ -15,6 +15,8 @@ computes, written from the paper's definitions (arXiv 2609.32398):
 * ``surrogate``       -- Sec. 3.1.3, Eq. (6)-(7): the surrogate loss
   (scale/(N^2 k)) sum_ij G_ij C_ij, C_ij = sum_t p_it (f_it - f_jt), and its
   gradient with respect to the routing probabilities (G, F detached).
+* ``surrogate_loss_blocked`` -- the same loss with the token sums inside C
+  taken by a numpy matrix product, for inputs of millions of tokens.
 * ``load_stats``      -- per-expert loads n_i (App. C.3), the Local-LBL loss
   sum_i f_i P_i of Sec. 4.2 and MaxVio (App. E) over a rank placement.
 
@@ -35,6 +37,7 @@ _LIB_PATH = os.path.join(_HERE, "liboracle.so")
 _lib = None
 
 F32, BF16 = 0, 1
+CFLAGS = ["-O3", "-fPIC", "-shared", "-fopenmp", "-std=c11"]
 
 
 class _LossResult(ctypes.Structure):
@@ -48,12 +51,12 @@ class _LoadStatsResult(ctypes.Structure):
 
 
 def build(force: bool = True) -> str:
-    """Compile the oracle with gcc (-O2, OpenMP; portable x86-64 code)."""
+    """Compile the oracle with gcc (-O3, OpenMP; portable x86-64 code, no -march)."""
     global _lib
     if not force and os.path.exists(_LIB_PATH):
         return _LIB_PATH
     tmp = _LIB_PATH + ".tmp"
-    subprocess.run(["gcc", "-O2", "-fPIC", "-shared", "-fopenmp", "-std=c11", _SRC, "-o", tmp, "-lm"], check=True)
+    subprocess.run(["gcc", *CFLAGS, _SRC, "-o", tmp, "-lm"], check=True)
     os.replace(tmp, _LIB_PATH)
     _lib = None
     return _LIB_PATH
@@ -156,6 +159,29 @@ def surrogate(p: np.ndarray, F: np.ndarray, G: np.ndarray, k: int, scale: float 
     if rc:
         raise ValueError(f"oracle_surrogate: bad arguments N={N} E={E} k={k}")
     return float(loss.value), grad
+
+
+def surrogate_loss_blocked(p: np.ndarray, F: np.ndarray, G: np.ndarray, k: int, scale: float = 1.0,
+                           block: int = 1 << 18) -> float:
+    """Eq. (7) loss alone for large N: the same definition as ``surrogate``,
+    with the sum over tokens inside C_ij taken by a library matrix product.
+    C_ij = sum_t p_it f_it - sum_t p_it f_jt = a_i - B_ij, where a_i is the
+    probability mass expert i receives from its own tokens and B = (F p)^T
+    (fp64, accumulated over blocks of tokens).  Then
+    loss = scale / (N^2 k) * sum_ij G_ij C_ij."""
+    N, E = p.shape
+    assert F.shape == (E, N) and G.shape == (E, E)
+    a = np.zeros(E, dtype=np.float64)
+    B = np.zeros((E, E), dtype=np.float64)
+    for t0 in range(0, N, block):
+        pb = np.ascontiguousarray(p[t0:t0 + block])
+        pb = (pb.astype(np.uint32) << 16).view(np.float32) if pb.dtype == np.uint16 else pb
+        pb = pb.astype(np.float64)
+        Fb = F[:, t0:t0 + block].astype(np.float64)
+        a += (pb * Fb.T).sum(axis=0)
+        B += (Fb @ pb).T
+    C = a[:, None] - B
+    return float(scale / (float(N) * float(N) * k) * (G.astype(np.float64) * C).sum())
 
 
 def load_stats(F: np.ndarray, k: int, p: np.ndarray | None = None, rank=None, R: int = 0):

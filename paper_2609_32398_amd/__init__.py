@@ -27,6 +27,7 @@ from .hipbuild import LIB_PATH, build  # noqa: F401
 
 DO_OK, DO_ERR_INVALID_ARG, DO_ERR_UNSUPPORTED_DTYPE, DO_ERR_CAPACITY, DO_ERR_OVERFLOW, DO_ERR_HIP = range(6)
 DO_F32, DO_BF16 = 0, 1
+DO_OPT_SCHEDULE, DO_OPT_GRAM = 0, 1
 
 LOSS_RESULT_BYTES = 40
 LOSS_FIELDS = ("sum", "sumsq", "loss", "mean", "var")
@@ -71,6 +72,7 @@ def lib():
             "do_last_error": ([], ctypes.c_char_p),
             "do_version": ([], i32),
             "do_profile_next": ([vp, vp], st),
+            "do_set_option": ([st, i32], st),
         }
         for name, (args, res) in sigs.items():
             f = getattr(L, name)
@@ -112,16 +114,55 @@ def _dtype_code(t: torch.Tensor) -> int:
     raise TypeError(f"unsupported score dtype {t.dtype}")
 
 
-def _scores_3d(scores: torch.Tensor):
-    if not scores.is_cuda:
-        raise ValueError("scores must be a device tensor")
-    if not scores.is_contiguous():
-        raise ValueError("scores must be contiguous")
+def _want(t: torch.Tensor, name: str, shape=None, dtypes=None, numel=None):
+    """Checks a tensor argument before its pointer reaches the library: shape
+    (or element count), dtype and contiguity first, then that it lives on the
+    current GPU.  Every failure raises ValueError before any launch."""
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name} must be a torch.Tensor")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if numel is not None and t.numel() < numel:
+        raise ValueError(f"{name} holds {t.numel()} elements, at least {numel} are needed")
+    if dtypes is not None and t.dtype not in dtypes:
+        raise ValueError(f"{name} has dtype {t.dtype}, expected one of {dtypes}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    why = _device_problem(t)
+    if why:
+        raise ValueError(f"{name} {why}")
+
+
+def _device_problem(t: torch.Tensor) -> str | None:
+    """Why `t` cannot be handed to the library as device memory, or None."""
+    if not t.is_cuda:
+        return "must be a device tensor"
+    if t.device.index != torch.cuda.current_device():
+        return f"is on {t.device}, not on the current device"
+    return None
+
+
+_SCORE_DTYPES = (torch.float32, torch.bfloat16)
+_I64, _I32, _U8 = (torch.int64,), (torch.int32,), (torch.uint8,)
+
+
+def _scores_3d(scores: torch.Tensor, name: str = "scores"):
+    if not isinstance(scores, torch.Tensor) or scores.dim() not in (2, 3):
+        raise ValueError(f"{name} must be a tensor of shape [N, E] or [L, N, E]")
+    _want(scores, name, dtypes=_SCORE_DTYPES)
     if scores.dim() == 2:
         return 1, scores.shape[0], scores.shape[1]
-    if scores.dim() == 3:
-        return scores.shape[0], scores.shape[1], scores.shape[2]
-    raise ValueError("scores must be [N, E] or [L, N, E]")
+    return scores.shape[0], scores.shape[1], scores.shape[2]
+
+
+def _words(N: int) -> int:
+    return (N + 63) // 64
+
+
+def set_option(option: int, value: int):
+    """do_set_option: process-wide override of a choice that never changes results
+    (DO_OPT_SCHEDULE: -1 tuned, 0 XCD-partitioned, 1 contiguous; DO_OPT_GRAM: 0 MFMA, 1 popcount)."""
+    _check(lib().do_set_option(int(option), int(value)), "do_set_option")
 
 
 def loss_records(out: torch.Tensor) -> list[dict]:
@@ -151,27 +192,38 @@ def do_topk_signature(scores: torch.Tensor, k: int, bits: torch.Tensor | None = 
     L, N, E = _scores_3d(scores)
     if bits is None:
         bits = alloc_bits(L, N, E, scores.device)
+    _want(bits, "bits", numel=L * E * _words(N), dtypes=_I64)
     _check(lib().do_topk_signature(scores.data_ptr(), _dtype_code(scores), N, E, k, L, bits.data_ptr(), _stream()),
            "do_topk_signature")
     return bits
 
 
 def do_pairwise_hamming(bits: torch.Tensor, N: int, D: torch.Tensor | None = None) -> torch.Tensor:
+    if not isinstance(bits, torch.Tensor) or bits.dim() not in (2, 3):
+        raise ValueError("bits must be a tensor of shape [E, W] or [L, E, W]")
     if bits.dim() == 2:
         bits = bits.unsqueeze(0)
-    L, E, _ = bits.shape
+    L, E, W = bits.shape
+    if W != _words(N):
+        raise ValueError(f"bits has {W} words per expert, ceil(N/64) = {_words(N)} for N = {N}")
+    _want(bits, "bits", dtypes=_I64)
     if D is None:
         D = alloc_D(L, E, bits.device)
+    _want(D, "D", numel=L * E * E, dtypes=_I32)
     _check(lib().do_pairwise_hamming(bits.data_ptr(), N, E, L, D.data_ptr(), _stream()), "do_pairwise_hamming")
     return D
 
 
 def do_loss(D: torch.Tensor, out: torch.Tensor | None = None) -> torch.Tensor:
+    if not isinstance(D, torch.Tensor) or D.dim() not in (2, 3) or D.shape[-1] != D.shape[-2]:
+        raise ValueError("D must be a tensor of shape [E, E] or [L, E, E]")
     if D.dim() == 2:
         D = D.unsqueeze(0)
     L, E, _ = D.shape
+    _want(D, "D", dtypes=_I32)
     if out is None:
         out = alloc_out(L, D.device)
+    _want(out, "out", numel=L * LOSS_RESULT_BYTES, dtypes=_U8)
     _check(lib().do_loss(D.data_ptr(), E, L, out.data_ptr(), _stream()), "do_loss")
     return out
 
@@ -185,6 +237,10 @@ def do_fused(scores: torch.Tensor, k: int, want_bits: bool = False, bits: torch.
         D = alloc_D(L, E, scores.device)
     if out is None:
         out = alloc_out(L, scores.device)
+    if bits is not None:
+        _want(bits, "bits", numel=L * E * _words(N), dtypes=_I64)
+    _want(D, "D", numel=L * E * E, dtypes=_I32)
+    _want(out, "out", numel=L * LOSS_RESULT_BYTES, dtypes=_U8)
     _check(lib().do_fused(scores.data_ptr(), _dtype_code(scores), N, E, k, L,
                           bits.data_ptr() if bits is not None else None, D.data_ptr(), out.data_ptr(), _stream()),
            "do_fused")
@@ -194,11 +250,16 @@ def do_fused(scores: torch.Tensor, k: int, want_bits: bool = False, bits: torch.
 def do_surrogate(p: torch.Tensor, k: int, bits: torch.Tensor, D: torch.Tensor, scale: float = 1.0,
                  want_grad: bool = True, loss: torch.Tensor | None = None, grad: torch.Tensor | None = None):
     """Eq. (7) surrogate loss per layer (float64 [L]) and dloss/dp (float32 [L, N, E] or None)."""
-    L, N, E = _scores_3d(p)
+    L, N, E = _scores_3d(p, "p")
+    _want(bits, "bits", numel=L * E * _words(N), dtypes=_I64)
+    _want(D, "D", numel=L * E * E, dtypes=_I32)
     if loss is None:
         loss = torch.empty(L, dtype=torch.float64, device=p.device)
     if want_grad and grad is None:
         grad = torch.empty((L, N, E), dtype=torch.float32, device=p.device)
+    _want(loss, "loss", numel=L, dtypes=(torch.float64,))
+    if grad is not None:
+        _want(grad, "grad", numel=L * N * E, dtypes=(torch.float32,))
     _check(lib().do_surrogate(p.data_ptr(), _dtype_code(p), N, E, k, L, bits.data_ptr(), D.data_ptr(), float(scale),
                               loss.data_ptr(), grad.data_ptr() if grad is not None else None, _stream()),
            "do_surrogate")
@@ -213,21 +274,36 @@ def do_load_stats(bits: torch.Tensor, N: int, k: int, p: torch.Tensor | None = N
     `bits_ptr` with E and L given, e.g. a stream history).  p: routing probabilities [L, N, E] or
     None; expert_rank: host sequence of E ranks in [0, R) or None (one expert per rank)."""
     if bits_ptr is None:
+        if not isinstance(bits, torch.Tensor) or bits.dim() not in (2, 3):
+            raise ValueError("bits must be a tensor of shape [E, W] or [L, E, W]")
         if bits.dim() == 2:
             bits = bits.unsqueeze(0)
         L, E = bits.shape[0], bits.shape[1]
+        if bits.shape[2] < max(ld, _words(N)):
+            raise ValueError(f"bits has {bits.shape[2]} words per expert, fewer than {max(ld, _words(N))}")
+        _want(bits, "bits", dtypes=_I64)
         ptr = bits.data_ptr()
         dev = bits.device
     else:
+        if E is None or L is None:
+            raise ValueError("bits_ptr needs E and L")
         ptr = bits_ptr
         dev = torch.device("cuda", torch.cuda.current_device())
     if loads is None:
         loads = torch.empty((L, E), dtype=torch.int32, device=dev)
     if out is None:
         out = torch.empty((L, LOAD_STATS_BYTES), dtype=torch.uint8, device=dev)
+    _want(loads, "loads", numel=L * E, dtypes=_I32)
+    _want(out, "out", numel=L * LOAD_STATS_BYTES, dtypes=_U8)
     rk = None
     if expert_rank is not None:
+        if len(expert_rank) != E:
+            raise ValueError(f"expert_rank has {len(expert_rank)} entries, expected E = {E}")
         rk = (ctypes.c_int32 * E)(*[int(r) for r in expert_rank])
+    if p is not None:
+        _want(p, "p", shape=(L, N, E) if p.dim() == 3 else (N, E), dtypes=_SCORE_DTYPES)
+        if p.dim() == 2 and L != 1:
+            raise ValueError("p of shape [N, E] needs L = 1")
     pptr, pdt = (p.data_ptr(), _dtype_code(p)) if p is not None else (None, DO_F32)
     _check(lib().do_load_stats(ptr, N, ld, E, k, L, pptr, pdt, rk, R, loads.data_ptr(), out.data_ptr(), _stream()),
            "do_load_stats")
@@ -261,23 +337,38 @@ class DoStream:
         _check(lib().do_stream_create(E, k, capacity_tokens, ctypes.byref(h)), "do_stream_create")
         self.h, self.E, self.k, self.capacity = h, E, k, capacity_tokens
 
+    def _micro_batch(self, scores: torch.Tensor, name: str = "scores") -> int:
+        if not isinstance(scores, torch.Tensor) or scores.dim() != 2:
+            raise ValueError(f"{name} must be a tensor of shape [n_tokens, E]")
+        if scores.shape[1] != self.E:
+            raise ValueError(f"{name} has {scores.shape[1]} experts, the history has E = {self.E}")
+        _want(scores, name, dtypes=_SCORE_DTYPES)
+        return scores.shape[0]
+
     def append(self, scores: torch.Tensor):
-        _, N, E = _scores_3d(scores)
+        N = self._micro_batch(scores)
         _check(lib().do_stream_append(self.h, scores.data_ptr(), _dtype_code(scores), N, _stream()),
                "do_stream_append")
 
     def append_many(self, score_list):
+        if not 1 <= len(score_list) <= 64:
+            raise ValueError("append_many takes 1 to 64 micro-batches")
+        N = self._micro_batch(score_list[0], "scores[0]")
+        for i, t in enumerate(score_list[1:], 1):
+            self._micro_batch(t, f"scores[{i}]")
+            if t.shape != score_list[0].shape or t.dtype != score_list[0].dtype:
+                raise ValueError(f"scores[{i}] differs in shape or dtype from scores[0]")
         ptrs = (ctypes.c_void_p * len(score_list))(*[s.data_ptr() for s in score_list])
-        _, N, _ = _scores_3d(score_list[0])
         _check(lib().do_stream_append_many(self.h, ptrs, _dtype_code(score_list[0]), N, len(score_list), _stream()),
                "do_stream_append_many")
 
     def finalize(self, D: torch.Tensor | None = None, out: torch.Tensor | None = None):
-        dev = torch.device("cuda", torch.cuda.current_device())
         if D is None:
-            D = torch.empty((self.E, self.E), dtype=torch.int32, device=dev)
+            D = torch.empty((self.E, self.E), dtype=torch.int32, device=torch.cuda.current_device())
         if out is None:
-            out = alloc_out(1, dev)
+            out = alloc_out(1, torch.device("cuda", torch.cuda.current_device()))
+        _want(D, "D", numel=self.E * self.E, dtypes=_I32)
+        _want(out, "out", numel=LOSS_RESULT_BYTES, dtypes=_U8)
         _check(lib().do_stream_finalize(self.h, D.data_ptr(), out.data_ptr(), _stream()), "do_stream_finalize")
         return D, out
 

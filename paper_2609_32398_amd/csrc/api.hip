@@ -143,6 +143,11 @@ DOLOSS_API const char* do_last_error(void) { return g_last_error.c_str(); }
 
 DOLOSS_API int32_t do_version(void) { return 100; }
 
+DOLOSS_API do_status do_set_option(do_option opt, int32_t value) {
+  if (!dol::set_option((int)opt, value)) return fail(DO_ERR_INVALID_ARG, "unknown option or value out of range");
+  return DO_OK;
+}
+
 DOLOSS_API do_status do_profile_next(hipEvent_t start, hipEvent_t stop) {
   g_prof_start = start;
   g_prof_stop = stop;

@@ -84,8 +84,10 @@ hipError_t launch_gram_bits(const u64* bits, int64_t W, int32_t E, int32_t L, ui
 // The same Gram on fp4 MFMA tiles (E <= 256): counts added into cacc [L][E][E]
 // (upper triangle, zeroed by the caller).
 hipError_t launch_gram_mfma(const u64* bits, int64_t W, int32_t E, int32_t L, uint32_t* cacc, hipStream_t s);
-// False when DOLOSS_GRAM selects the popcount Gram (a comparison switch).
+// False when do_set_option selects the popcount Gram (a comparison switch).
 bool gram_mfma_enabled();
+// do_set_option: false for an unknown option or a value out of range.
+bool set_option(int opt, int value);
 
 // D = c_ii + c_jj - 2 c_ij (symmetric, zero diagonal); out (nullable) = loss.
 // cacc may alias D.

@@ -143,9 +143,13 @@ __device__ __forceinline__ void mul128(u64 a, u64 b, u64& hi, u64& lo) {
   hi = __umul64hi(a, b);
 }
 
-// Fill one loss record from exact sums over the E(E-1) off-diagonal entries.
-__device__ void write_result(do_loss_result* o, u64 s1, u64 s2, int E) {
+// Fill one loss record from exact sums over the E(E-1) off-diagonal entries;
+// the sum of squares is the 128-bit (s2h, s2l).  Entries are below 2^32 and
+// E <= 1024, so S1 < 2^52, S2 < 2^84 and P*S2, S1^2 < 2^104.  sumsq saturates
+// at 2^64 - 1 when S2 does not fit 64 bits; loss is always S2 rounded to fp64.
+__device__ void write_result(do_loss_result* o, u64 s1, u64 s2h, u64 s2l, int E) {
   if (E < 2) {
+    (void)s2h;
     o->sum = 0;
     o->sumsq = 0;
     o->loss = 0.0;
@@ -155,12 +159,13 @@ __device__ void write_result(do_loss_result* o, u64 s1, u64 s2, int E) {
   }
   const u64 P = (u64)E * (u64)(E - 1);
   o->sum = s1;
-  o->sumsq = s2;
-  o->loss = (double)s2;
+  o->sumsq = s2h != 0ull ? ~0ull : s2l;
+  o->loss = s2h != 0ull ? (double)s2h * 18446744073709551616.0 + (double)s2l : (double)s2l;
   o->mean = (double)s1 / (double)P;
-  // population variance = (P*s2 - s1^2) / P^2 with an exact 128-bit numerator
+  // population variance = (P*S2 - S1^2) / P^2 with an exact 128-bit numerator
   u64 ah, al, bh, bl;
-  mul128(P, s2, ah, al);
+  mul128(P, s2l, ah, al);
+  ah += P * s2h;
   mul128(s1, s1, bh, bl);
   const u64 nl = al - bl;
   const u64 nh = ah - bh - (al < bl ? 1ull : 0ull);
@@ -250,7 +255,7 @@ __global__ __launch_bounds__(1024) void k_finalize(const uint32_t* cacc, uint32_
   }
   if (out == nullptr) return;
   block_sum2(s1, s2);
-  if (threadIdx.x == 0) write_result(out + blockIdx.x, s1, s2, E);
+  if (threadIdx.x == 0) write_result(out + blockIdx.x, s1, 0ull, s2, E);
 }
 
 constexpr int kSplitRows = 8;  // rows per block of the split finalize, one per wave
@@ -299,7 +304,7 @@ __global__ __launch_bounds__(512) void k_finalize_split(const uint32_t* __restri
     if (atomicAdd(&fin[2], 1ull) == (u64)gridDim.x - 1) {
       __threadfence();
       const u64 S1 = atomicAdd(&fin[0], 0ull), S2 = atomicAdd(&fin[1], 0ull);
-      write_result(out, S1, S2, E);
+      write_result(out, S1, 0ull, S2, E);
       atomicExch(&fin[0], 0ull);
       atomicExch(&fin[1], 0ull);
       atomicExch(&fin[2], 0ull);
@@ -307,12 +312,48 @@ __global__ __launch_bounds__(512) void k_finalize_split(const uint32_t* __restri
   }
 }
 
+// (hi, lo) += (bh, bl) in 128 bits.
+__device__ __forceinline__ void add128(u64& hi, u64& lo, u64 bh, u64 bl) {
+  lo += bl;
+  hi += bh + (lo < bl ? 1ull : 0ull);
+}
+
+// Sum of (s1, s2h:s2l) across the block; valid in thread 0.
+__device__ void block_sum3(u64& s1, u64& s2h, u64& s2l) {
+  __shared__ u64 part[3][16];
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    s1 += __shfl_xor(s1, off, 64);
+    add128(s2h, s2l, __shfl_xor(s2h, off, 64), __shfl_xor(s2l, off, 64));
+  }
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int nw = (blockDim.x + 63) >> 6;
+  if (lane == 0) {
+    part[0][wave] = s1;
+    part[1][wave] = s2h;
+    part[2][wave] = s2l;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    u64 a = 0, h = 0, l = 0;
+    for (int i = 0; i < nw; ++i) {
+      a += part[0][i];
+      add128(h, l, part[1][i], part[2][i]);
+    }
+    s1 = a;
+    s2h = h;
+    s2l = l;
+  }
+}
+
 // Sums of a stored D (every off-diagonal entry), 8 rows per wave per pass.
+// Entries are arbitrary u32 values, so the sum of squares is kept in 128
+// bits per lane (one entry's square alone may reach 2^64 - 2^33 + 1).
 __global__ __launch_bounds__(1024) void k_loss(const uint32_t* D, do_loss_result* out, int E) {
   const int64_t EE = (int64_t)E * E;
   const uint32_t* d = D + blockIdx.x * EE;
   const int nw = (int)(blockDim.x >> 6), w = (int)(threadIdx.x >> 6), lane = (int)(threadIdx.x & 63);
-  u64 s1 = 0, s2 = 0;
+  u64 s1 = 0, s2h = 0, s2l = 0;
   // as in k_finalize: 16 loads per lane (8 rows x 2 column blocks) per round
   // trip, 32-bit offsets, positions off the matrix or on the diagonal read
   // entry 0 and count as zero
@@ -334,13 +375,13 @@ __global__ __launch_bounds__(1024) void k_loss(const uint32_t* D, do_loss_result
 #pragma unroll
         for (int r = 0; r < kFinRows; ++r) {
           s1 += dv[q][r];
-          s2 += (u64)dv[q][r] * (u64)dv[q][r];
+          add128(s2h, s2l, 0ull, (u64)dv[q][r] * (u64)dv[q][r]);
         }
       }
     }
   }
-  block_sum2(s1, s2);
-  if (threadIdx.x == 0) write_result(out + blockIdx.x, s1, s2, E);
+  block_sum3(s1, s2h, s2l);
+  if (threadIdx.x == 0) write_result(out + blockIdx.x, s1, s2h, s2l, E);
 }
 
 }  // namespace

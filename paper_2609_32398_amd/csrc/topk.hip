@@ -29,13 +29,18 @@
 // +-0, +-inf or NaN, or is not positive under positive keys, is re-ranked by
 // an exact per-lane fallback on 64-bit keys.
 //
-// Gram.  mode 2 (default): int8 MFMA (32x32x32 at 256 experts, 16x16x64
-// below) on 0/1 bytes expanded from the signature words, up to five expert
-// tile pairs per wave, accumulators in registers.  mode 1: VALU
+// Gram.  Default: scaled fp4 (e2m1) MFMA, v_mfma_scale_f32_32x32x64_f8f6f4 at
+// 256 experts and v_mfma_scale_f32_16x16x128_f8f6f4 below, on operands
+// expanded from the signature words (one nibble per token, 0.5 or 0, block
+// scale 2^1 on both sides so that every co-occurrence adds exactly 1.0); up
+// to five expert tile pairs per wave, fp32 accumulators in registers, exact
+// while a count stays below 2^24 (a block flushes at the latest every 32,767
+// units of 512 tokens).  Alternative (do_set_option DO_OPT_GRAM = 1): VALU
 // popcount(a & b) on 4x4 micro-tiles per thread.  Either way a block adds its
 // integer partial counts into the accumulator matrix when the layer changes
 // and at the end (order-independent).
 #include <algorithm>
+#include <atomic>
 #include <cstdio>
 #include <cstdlib>
 #include <mutex>
@@ -591,8 +596,8 @@ typedef unsigned long long v2u64 __attribute__((ext_vector_type(2)));
 // after each ranked chunk), so they overlap other waves' ranking instead of
 // following every barrier at once.  Gram accumulators are flushed when the
 // layer changes and at the end.  flags bit 0: fast path allowed (16-byte
-// rows, k <= 8, E <= 256); bit 1: XCD-adjacent group placement.  gu: units
-// per schedule group.
+// rows, k <= 8, E <= 256); bit 1: XCD-partitioned schedule.  gu: units per
+// schedule group.
 // ---------------------------------------------------------------------------
 template <typename T, int EP, int GM>
 __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, const PathArgs a, int flags, int64_t gu) {
@@ -616,23 +621,21 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
   // Unit schedule: the unit range [lo, hi) of a block's partition is cut into
   // groups of `gu` consecutive units, and the Gs blocks of the partition take
   // groups pos, pos + Gs, pos + 2 Gs, ...  Contiguous ranges are the case of
-  // one group per block.  flags bits 1-2 select the partition and placement:
+  // one group per block.  flags bit 1 selects the partition:
   //   0: one partition [0, U), pos = b
-  //   1: one partition, blocks that share an XCD (round-robin dispatch:
-  //      b mod 8) on adjacent groups
-  //   2: eight partitions, one per XCD (b mod 8), of U/8 units each; the
-  //      XCD's blocks work on adjacent groups of its partition, so their
-  //      signature stores land side by side while each block stays in few
-  //      layers (few Gram flushes, and those of different XCDs go to
-  //      different layers)
+  //   1: eight partitions, one per XCD (blocks are dispatched round-robin,
+  //      so block b runs on XCD b mod 8), of U/8 units each; the XCD's
+  //      blocks work on adjacent groups of its partition, so their signature
+  //      stores land side by side while each block stays in few layers (few
+  //      Gram flushes, and those of different XCDs go to different layers)
   const int64_t U = tab->tile_start[tab->nseg];
   const int G = gridDim.x;
   const int b = blockIdx.x;
-  const int smode = (G & 7) == 0 ? (flags >> 1) & 3 : 0;
-  const int64_t lo = smode == 2 ? (int64_t)(b & 7) * U / 8 : 0;
-  const int64_t hi = smode == 2 ? (int64_t)((b & 7) + 1) * U / 8 : U;
-  const int Gs = smode == 2 ? G >> 3 : G;
-  const int pos = smode == 2 ? b >> 3 : smode == 1 ? (b & 7) * (G >> 3) + (b >> 3) : b;
+  const bool xcd = (G & 7) == 0 && (flags & 2) != 0;
+  const int64_t lo = xcd ? (int64_t)(b & 7) * U / 8 : 0;
+  const int64_t hi = xcd ? (int64_t)((b & 7) + 1) * U / 8 : U;
+  const int Gs = xcd ? G >> 3 : G;
+  const int pos = xcd ? b >> 3 : b;
   const int64_t ug = lo + (int64_t)pos * gu;
   if (ug >= hi) return;
   // unit after u in this block's schedule (U when there is none)
@@ -1039,36 +1042,19 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
   flush(pend.layer);
 }
 
-// kGramPopc or kGramMfma, read once from DOLOSS_GRAM ("popc" selects popcount);
-// a function-local static, so concurrent first calls are safe
-int gram_mode() {
-  static const int mode = [] {
-    const char* v = getenv("DOLOSS_GRAM");
-    return (v != nullptr && v[0] == 'p') ? kGramPopc : kGramMfma;
-  }();
-  return mode;
-}
+// Process-wide overrides of choices that never change results (do_set_option):
+// the Gram kind and the unit schedule.
+std::atomic<int> g_opt_gram{0};    // 0: fp4 MFMA, 1: VALU popcount
+std::atomic<int> g_opt_sched{-1};  // -1: measured per launch shape, else an index into kSchedCand
 
-// Unit schedule of the Top-K kernel.  gu < 0: chosen per launch
-// (tuned_schedule); DOLOSS_SCHED fixes it instead: "c" = one contiguous range per
-// block, "i<n>" / "x<n>" / "p<n>" = groups of n units in placement mode 0 / 1
-// / 2 (see k_topk).
+int gram_mode() { return g_opt_gram.load(std::memory_order_relaxed) == 1 ? kGramPopc : kGramMfma; }
+
+// Unit schedule of the Top-K kernel: groups of gu consecutive units (gu = 0:
+// one contiguous range per block), in one partition or one per XCD.
 struct Sched {
   int64_t gu;
-  int mode;
+  bool xcd;
 };
-Sched schedule() {
-  static const Sched sched = [] {  // read once (thread-safe initialisation)
-    const char* v = getenv("DOLOSS_SCHED");
-    if (v != nullptr && v[0] == 'c') return Sched{0, 0};
-    if (v != nullptr && (v[0] == 'i' || v[0] == 'x' || v[0] == 'p')) {
-      const int n = atoi(v + 1);
-      return Sched{n > 0 ? n : 4, v[0] == 'i' ? 0 : v[0] == 'x' ? 1 : 2};
-    }
-    return Sched{-1, 0};
-  }();
-  return sched;
-}
 
 template <typename T, int EP, int GM>
 hipError_t launch_one(const SegTable& tab, const PathArgs& a, bool fast, Sched sc, hipStream_t s) {
@@ -1085,10 +1071,10 @@ hipError_t launch_one(const SegTable& tab, const PathArgs& a, bool fast, Sched s
   int64_t blocks = std::min<int64_t>((int64_t)di.cu_count * occ, units);
   blocks = std::max<int64_t>(blocks, 1);
   int64_t gu = sc.gu;
-  const int64_t per_part = sc.mode == 2 ? (units + 7) / 8 : units;
-  const int64_t gs = sc.mode == 2 ? std::max<int64_t>(blocks / 8, 1) : blocks;
+  const int64_t per_part = sc.xcd ? (units + 7) / 8 : units;
+  const int64_t gs = sc.xcd ? std::max<int64_t>(blocks / 8, 1) : blocks;
   if (gu <= 0 || gu * gs > per_part) gu = (per_part + gs - 1) / gs;  // contiguous ranges
-  const int flags = (fast ? 1 : 0) | (sc.mode << 1);
+  const int flags = (fast ? 1 : 0) | (sc.xcd ? 2 : 0);
   hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kFusedThreads), lds, s, tab, a, flags, gu);
   return hipGetLastError();
 }
@@ -1122,8 +1108,10 @@ hipError_t launch_ep(const SegTable& tab, const PathArgs& a, bool fast, Sched sc
 // which never waits, and once every candidate has one, the fastest is used
 // for all later launches of that shape.  The very first launch of a shape is
 // not measured (cold caches and TLB).  Launches under stream capture and
-// launches below kTuneMinUnits use the first candidate.
-constexpr Sched kSchedCand[2] = {Sched{4, 2}, Sched{0, 0}};  // XCD partitions; contiguous ranges
+// launches below kTuneMinUnits use the first candidate (or the one already
+// chosen for the shape); a capture never touches the measurement events.
+// When every slot of the table holds a shape, a decided one is recycled.
+constexpr Sched kSchedCand[2] = {Sched{4, true}, Sched{0, false}};  // XCD partitions; contiguous ranges
 constexpr int kNumCand = 2;
 constexpr int64_t kTuneMinUnits = 8192;  // 4 Mi tokens
 constexpr int kTuneSlots = 16;
@@ -1140,10 +1128,25 @@ struct Tune {
 std::mutex g_tune_mu;
 Tune g_tune[kTuneSlots];
 int g_ntune = 0;
+int g_tune_next = 0;  // next slot considered for recycling
 
 uint64_t mix(uint64_t h, uint64_t v) {
   h ^= v + 0x9E3779B97F4A7C15ull + (h << 6) + (h >> 2);
   return h;
+}
+
+void release_events(Tune& t) {
+  for (int c = 0; c < kNumCand; ++c)
+    for (int i = 0; i < 2; ++i)
+      if (t.ev[c][i] != nullptr) {
+        (void)hipEventDestroy(t.ev[c][i]);
+        t.ev[c][i] = nullptr;
+      }
+}
+
+void decide(Tune& t, int c) {
+  t.chosen = c;
+  release_events(t);  // no trial is pending once a candidate is chosen
 }
 
 // Picks the schedule of one launch and, when it is a measured trial, sets
@@ -1170,16 +1173,27 @@ Sched tuned_schedule(do_dtype dt, const SegTable& tab, const PathArgs& a, bool f
   Tune* t = nullptr;
   for (int i = 0; i < g_ntune; ++i)
     if (g_tune[i].key == key && g_tune[i].device == dev) t = &g_tune[i];
+  if (t != nullptr && t->chosen >= 0) return kSchedCand[t->chosen];
+  if (capturing) return kSchedCand[0];
   if (t == nullptr) {
-    if (g_ntune == kTuneSlots) return kSchedCand[0];
-    t = &g_tune[g_ntune++];
+    if (g_ntune < kTuneSlots) {
+      t = &g_tune[g_ntune++];
+    } else {
+      for (int i = 0; i < kTuneSlots && t == nullptr; ++i) {
+        Tune& c = g_tune[(g_tune_next + i) % kTuneSlots];
+        if (c.chosen >= 0) {
+          t = &c;
+          g_tune_next = (g_tune_next + i + 1) % kTuneSlots;
+        }
+      }
+      if (t == nullptr) return kSchedCand[0];  // every slot is still measuring
+    }
     *t = Tune{};
     t->key = key;
     t->device = dev;
     t->chosen = -1;
     for (int c = 0; c < kNumCand; ++c) t->best[c] = -1.f;
   }
-  if (t->chosen >= 0) return kSchedCand[t->chosen];
   // collect finished trials
   bool all = true;
   for (int c = 0; c < kNumCand; ++c) {
@@ -1191,7 +1205,8 @@ Sched tuned_schedule(do_dtype dt, const SegTable& tab, const PathArgs& a, bool f
           t->best[c] = t->best[c] < 0.f ? ms : std::min(t->best[c], ms);
         t->pending[c] = false;
       } else if (q != hipErrorNotReady) {
-        t->chosen = 0;  // measurement failed: keep the first candidate
+        t->pending[c] = false;
+        decide(*t, 0);  // measurement failed: keep the first candidate
         return kSchedCand[0];
       }
     }
@@ -1201,18 +1216,18 @@ Sched tuned_schedule(do_dtype dt, const SegTable& tab, const PathArgs& a, bool f
     int bc = 0;
     for (int c = 1; c < kNumCand; ++c)
       if (t->best[c] < 0.97f * t->best[bc]) bc = c;  // switch only for a clear gain
-    t->chosen = bc;
     if (getenv("DOLOSS_TUNE_LOG") != nullptr)
       fprintf(stderr, "[doloss] unit schedule for %lld units: candidates %.4f / %.4f ms, chose %d\n",
               (long long)units, t->best[0], t->best[1], bc);
+    decide(*t, bc);
     return kSchedCand[bc];
   }
-  if (capturing || t->calls++ == 0) return kSchedCand[0];
+  if (t->calls++ == 0) return kSchedCand[0];
   for (int c = 0; c < kNumCand; ++c) {
     if (t->best[c] > 0.f || t->pending[c]) continue;
     if (t->ev[c][0] == nullptr) {
       if (hipEventCreate(&t->ev[c][0]) != hipSuccess || hipEventCreate(&t->ev[c][1]) != hipSuccess) {
-        t->chosen = 0;
+        decide(*t, 0);
         return kSchedCand[0];
       }
     }
@@ -1309,9 +1324,9 @@ hipError_t launch_topk(do_dtype dt, SegTable& tab, int nseg, const PathArgs& a, 
   }
   if (tab.tile_start[nseg] == 0) return hipSuccess;
   const bool fast = fast_ok && a.k <= kFastMaxK && a.E <= kFastMaxE;
-  Sched sc = schedule();
   hipEvent_t ev[2] = {nullptr, nullptr};
-  if (sc.gu < 0) sc = tuned_schedule(dt, tab, a, fast, s, ev);
+  const int forced = g_opt_sched.load(std::memory_order_relaxed);
+  const Sched sc = forced >= 0 ? kSchedCand[forced] : tuned_schedule(dt, tab, a, fast, s, ev);
   if (ev[0] != nullptr) {
     const hipError_t e = hipEventRecord(ev[0], s);
     if (e != hipSuccess) return e;
@@ -1322,6 +1337,18 @@ hipError_t launch_topk(do_dtype dt, SegTable& tab, int nseg, const PathArgs& a, 
 }
 
 bool gram_mfma_enabled() { return gram_mode() == kGramMfma; }
+
+bool set_option(int opt, int value) {
+  if (opt == DO_OPT_SCHEDULE && value >= -1 && value < kNumCand) {
+    g_opt_sched.store(value, std::memory_order_relaxed);
+    return true;
+  }
+  if (opt == DO_OPT_GRAM && (value == 0 || value == 1)) {
+    g_opt_gram.store(value, std::memory_order_relaxed);
+    return true;
+  }
+  return false;
+}
 
 hipError_t launch_gram_mfma(const u64* bits, int64_t W, int32_t E, int32_t L, uint32_t* cacc, hipStream_t s) {
   if (E > kFastMaxE || W < 1) return hipErrorInvalidValue;

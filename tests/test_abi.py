@@ -163,3 +163,92 @@ def test_binding_requires_device_tensors(dl):
 
     with pytest.raises(ValueError):
         dl.do_topk_signature(torch.zeros(4, 8), 2)
+
+
+# ---------------------------------------------------------------------------
+# The binding checks every tensor argument before its pointer reaches the
+# library.  On this host the device predicate is replaced by one that accepts
+# CPU tensors, so the shape, dtype and size checks are reached; each bad
+# argument must raise ValueError, and no library call may happen (the library
+# entry points are replaced by a function that fails the test).
+# ---------------------------------------------------------------------------
+@pytest.fixture
+def host_binding(dl, monkeypatch):
+    import torch
+
+    monkeypatch.setattr(dl, "_device_problem", lambda t: None)
+
+    class NoCalls:
+        def __getattr__(self, name):
+            raise AssertionError(f"{name} was called although an argument is invalid")
+
+    monkeypatch.setattr(dl, "lib", lambda: NoCalls())
+    return dl, torch
+
+
+def test_binding_rejects_bad_tensors_before_any_call(host_binding):
+    dl, torch = host_binding
+    x = torch.zeros(100, 16)
+    bits = torch.zeros(1, 16, 2, dtype=torch.int64)
+    D = torch.zeros(1, 16, 16, dtype=torch.int32)
+    out = torch.zeros(1, 40, dtype=torch.uint8)
+    bad = [
+        lambda: dl.do_topk_signature(torch.zeros(100, 16, dtype=torch.float64), 2),     # score dtype
+        lambda: dl.do_topk_signature(torch.zeros(4, 100, 16).transpose(1, 2), 2),      # not contiguous
+        lambda: dl.do_topk_signature(torch.zeros(100), 2),                             # 1-D scores
+        lambda: dl.do_topk_signature(x, 2, bits=torch.zeros(1, 16, 1, dtype=torch.int64)),  # short bits
+        lambda: dl.do_topk_signature(x, 2, bits=bits.int()),                           # bits dtype
+        lambda: dl.do_fused(x, 2, bits=bits, D=torch.zeros(1, 16, 15, dtype=torch.int32), out=out),  # short D
+        lambda: dl.do_fused(x, 2, D=D, out=torch.zeros(1, 39, dtype=torch.uint8)),     # short out
+        lambda: dl.do_fused(x, 2, D=D.float(), out=out),                               # D dtype
+        lambda: dl.do_pairwise_hamming(bits, 200),                                     # N does not match W
+        lambda: dl.do_pairwise_hamming(bits, 100, D=torch.zeros(1, 16, 8, dtype=torch.int32)),  # short D
+        lambda: dl.do_loss(torch.zeros(16, 15, dtype=torch.int32)),                    # not square
+        lambda: dl.do_loss(D, out=torch.zeros(1, 8, dtype=torch.uint8)),               # short out
+        lambda: dl.do_surrogate(x, 2, torch.zeros(1, 16, 1, dtype=torch.int64), D),    # short bits
+        lambda: dl.do_surrogate(x, 2, bits, torch.zeros(1, 8, 8, dtype=torch.int32)),  # short D
+        lambda: dl.do_surrogate(x, 2, bits, D, grad=torch.zeros(100, 15)),             # short grad
+        lambda: dl.do_load_stats(bits, 200, 2),                                        # too few words for N
+        lambda: dl.do_load_stats(bits, 100, 2, p=torch.zeros(100, 15)),                # p of another E
+        lambda: dl.do_load_stats(bits, 100, 2, expert_rank=[0] * 15, R=1),             # rank map length
+        lambda: dl.do_load_stats(bits, 100, 2, loads=torch.zeros(1, 15, dtype=torch.int32)),  # short loads
+    ]
+    for i, f in enumerate(bad):
+        with pytest.raises(ValueError):
+            f()
+
+
+def test_stream_binding_rejects_bad_micro_batches(host_binding):
+    dl, torch = host_binding
+    s = dl.DoStream.__new__(dl.DoStream)  # a handle object without a library handle
+    s.h, s.E, s.k, s.capacity = None, 16, 2, 1000
+    with pytest.raises(ValueError):
+        s.append(torch.zeros(100, 8))                       # another expert count
+    with pytest.raises(ValueError):
+        s.append(torch.zeros(2, 100, 16))                   # 3-D scores
+    with pytest.raises(ValueError):
+        s.append_many([torch.zeros(100, 16), torch.zeros(90, 16)])  # unequal micro-batches
+    with pytest.raises(ValueError):
+        s.append_many([torch.zeros(100, 16), torch.zeros(100, 16, dtype=torch.bfloat16)])
+    with pytest.raises(ValueError):
+        s.append_many([])
+    with pytest.raises(ValueError):
+        s.finalize(torch.zeros(15, 15, dtype=torch.int32), torch.zeros(1, 40, dtype=torch.uint8))
+
+
+def test_set_option_rejects_unknown_values(dl):
+    L = dl.lib()
+    assert L.do_set_option(7, 0) == 1
+    assert L.do_set_option(0, 2) == 1     # schedule index out of range
+    assert L.do_set_option(0, -2) == 1
+    assert L.do_set_option(1, 2) == 1     # gram kind out of range
+    assert L.do_set_option(0, -1) == 0    # the defaults are accepted (and leave the state as it was)
+    assert L.do_set_option(1, 0) == 0
+
+
+def test_fused_without_bits_needs_e_at_most_256(dl):
+    # documented limit: bits may be NULL only for E <= 256 (wider E re-reads
+    # the stored signatures); E = 256 with NULL bits passes validation, so it
+    # is not called here (it would launch)
+    assert _st(dl, "do_fused", FAKE, 0, 64, 257, 8, 1, None, FAKE, FAKE, None) == 1
+    assert b"bits" in dl.lib().do_last_error()

@@ -2,13 +2,13 @@
 benchmark times (one do_fused call over all layers with signatures written;
 the stream as reset + one append_many of all micro-batches + finalize).
 
-Workloads 2 and 3 are compared with the oracle element by element in full.
-Workload 4 (8 x 4,194,304 tokens x 256 experts) is compared in full on its
-first and last layer; on every layer, sampled token positions are compared
-with the oracle's Top-K of those tokens and the properties that hold at any
-size are checked (Eq. 2 zero-sum, row sums, symmetry, exact loss of D).
-The surrogate loss (Eq. 7) runs on the same tokens: sampled gradients against
-the oracle and the loss against its linearity in p.
+Workloads 2, 3 and 4 are compared with the oracle element by element in full
+(every layer: signatures, distances, loss record).  The surrogate loss
+(Eq. 7) on workload 4 is compared with the oracle's loss on every layer, and
+sampled gradients with the oracle's gradient.  Every unit schedule the
+library can choose and both Gram kinds are run at full size and must give
+bit-identical results; so must repeated calls while the schedule tuner
+measures its candidates.
 """
 import numpy as np
 import pytest
@@ -29,6 +29,38 @@ def dl():
     return p
 
 
+def _same_results(dl, scores, k, ref, label):
+    """do_fused into fresh buffers must equal the oracle-checked `ref` bit for bit."""
+    bits, D, out = dl.do_fused(scores, k, want_bits=True)
+    torch.cuda.synchronize()
+    assert torch.equal(bits, ref[0]), f"{label}: signatures differ"
+    assert torch.equal(D, ref[1]), f"{label}: distances differ"
+    assert torch.equal(out, ref[2]), f"{label}: loss records differ"
+
+
+def _schedules_and_grams_agree(dl, scores, k, ref, name):
+    """Both fixed unit schedules, the popcount Gram, and five calls with the
+    run-time choice (the schedule tuner measures both candidates on the first
+    calls of a shape and then keeps one) all reproduce `ref`."""
+    try:
+        for opt, val, label in ((dl.DO_OPT_SCHEDULE, 0, "XCD-partitioned schedule"),
+                                (dl.DO_OPT_SCHEDULE, 1, "contiguous schedule")):
+            dl.set_option(opt, val)
+            print(f"[case] {name}: {label}", flush=True)
+            _same_results(dl, scores, k, ref, f"{name} {label}")
+        dl.set_option(dl.DO_OPT_SCHEDULE, -1)
+        dl.set_option(dl.DO_OPT_GRAM, 1)
+        print(f"[case] {name}: popcount Gram", flush=True)
+        _same_results(dl, scores, k, ref, f"{name} popcount Gram")
+        dl.set_option(dl.DO_OPT_GRAM, 0)
+        for rep in range(5):
+            print(f"[case] {name}: tuned call {rep}", flush=True)
+            _same_results(dl, scores, k, ref, f"{name} tuned call {rep}")
+    finally:
+        dl.set_option(dl.DO_OPT_SCHEDULE, -1)
+        dl.set_option(dl.DO_OPT_GRAM, 0)
+
+
 def test_workload2_full(dl, orc, syn):
     w = syn.WORKLOADS[2]
     L, N, E, k = w["layers"], w["n"], w["E"], w["k"]
@@ -36,7 +68,6 @@ def test_workload2_full(dl, orc, syn):
     scores, _ = upload_workload(syn, 2, L)
     bits, D, out = dl.do_fused(scores, k, want_bits=True)
     torch.cuda.synchronize()
-    del scores
     got_bits, got_D, recs = bits_np(bits), D_np(D), dl.loss_records(out)
     for l in range(L):
         x = syn.workload_fill(2, l)
@@ -50,6 +81,8 @@ def test_workload2_full(dl, orc, syn):
         assert len(idle) == 16 and not loads[idle].any()
         for i in idle:
             assert np.array_equal(got_D[l][i].astype(np.int64), np.where(np.arange(E) == i, 0, loads))
+    # 48 x 512 = 24,576 work units: the run-time schedule choice applies
+    _schedules_and_grams_agree(dl, scores, k, (bits, D, out), w["name"])
 
 
 def test_workload3_stream_full(dl, orc, syn):
@@ -74,64 +107,44 @@ def test_workload3_stream_full(dl, orc, syn):
         s.close()
 
 
-def _surrogate_full(dl, orc, syn, scores, bits, D, k):
-    """Eq. 7 on the full workload (its scores are per-token probabilities):
-    the gradient of sampled tokens against the oracle, and the loss against
-    sum_t sum_i p_it dloss/dp_it (the loss is linear in p)."""
-    L, N, E = scores.shape
-    print(f"[case] surrogate on the full workload L={L} N={N} E={E}", flush=True)
-    loss, grad = dl.do_surrogate(scores, k, bits, D)
-    torch.cuda.synchronize()
-    lin = [(scores[l].double() * grad[l].double()).sum().item() for l in range(L)]
-    loss = loss.cpu().numpy()
-    for l in range(L):
-        assert loss[l] == pytest.approx(lin[l], rel=1e-6), (l, loss[l], lin[l])
-    rng = np.random.default_rng(44)
-    Dh = D.cpu().numpy().view(np.uint32)
-    for l in (0, L - 1):
-        words = bits_np(bits[l])
-        tok = np.sort(rng.choice(N, 512, replace=False))
-        p = scores[l][torch.from_numpy(tok).cuda()].cpu().numpy()
-        F = bits_at(words, tok)
-        # the oracle's 1/(n^2 k) for n sampled tokens, rescaled to the full N
-        _, ref = orc.surrogate(p, F, Dh[l], k, scale=(len(tok) / N) ** 2)
-        got = grad[l][torch.from_numpy(tok).cuda()].cpu().numpy().astype(np.float64)
-        tol = 1e-5 * np.abs(ref) + 1e-6 * np.abs(ref).max()
-        assert (np.abs(got - ref) <= tol).all(), f"layer {l}: sampled gradients differ"
-    del grad
-    torch.cuda.empty_cache()
-
-
 def test_workload4_full(dl, orc, syn):
     w = syn.WORKLOADS[4]
     L, N, E, k = w["layers"], w["n"], w["E"], w["k"]
-    full = (0, L - 1)
     print(f"[case] {w['name']} full, L={L} N={N} E={E} k={k}", flush=True)
-    scores, kept = upload_workload(syn, 4, L, keep=full)
+    scores, _ = upload_workload(syn, 4, L)
     bits, D, out = dl.do_fused(scores, k, want_bits=True)
     torch.cuda.synchronize()
-    _surrogate_full(dl, orc, syn, scores, bits, D, k)
+    _schedules_and_grams_agree(dl, scores, k, (bits, D, out), w["name"])
+    # the surrogate loss (Eq. 7) and its gradient on the same tokens: the
+    # scores of this workload are per-token probabilities
+    print(f"[case] surrogate on the full workload L={L} N={N} E={E}", flush=True)
+    sloss, grad = dl.do_surrogate(scores, k, bits, D)
+    torch.cuda.synchronize()
+    sloss = sloss.cpu().numpy()
     del scores
     torch.cuda.empty_cache()
     recs = dl.loss_records(out)
     got_D = D_np(D)
-    rng = np.random.default_rng(4)
+    rng = np.random.default_rng(44)
     for l in range(L):
+        print(f"[case] {w['name']} layer {l}: full oracle", flush=True)
         words = bits_np(bits[l])
+        x = syn.workload_fill(4, l)
+        F, ref_bits, ref_D, ref_L = orc.run(x, k)
+        assert np.array_equal(words, ref_bits), f"layer {l}: signatures differ"
+        np.testing.assert_array_equal(got_D[l], ref_D, err_msg=f"layer {l}")
+        loss_close(recs[l], ref_L)
         check_invariants(words, got_D[l], recs[l], N, k, f"layer {l}")
-        # sampled tokens: the first and last words, and 64 random runs of 64 tokens
-        starts = np.concatenate([[0, N - 64], rng.integers(0, N - 64, 64)])
-        for t0 in starts:
-            x = syn.workload_fill(4, l, int(t0), 64)
-            F = orc.topk_signature(x, k)
-            tok = np.arange(t0, t0 + 64)
-            assert np.array_equal(bits_at(words, tok), F), f"layer {l}: tokens {t0}..{t0 + 63} differ"
-        if l in full:
-            print(f"[case] {w['name']} layer {l}: full oracle", flush=True)
-            F, ref_bits, ref_D, ref_L = orc.run(kept.pop(l), k)
-            assert np.array_equal(words, ref_bits), f"layer {l}: signatures differ"
-            np.testing.assert_array_equal(got_D[l], ref_D, err_msg=f"layer {l}")
-            loss_close(recs[l], ref_L)
+        # surrogate: the loss against the oracle's, sampled gradients against its gradient
+        ref_s = orc.surrogate_loss_blocked(x, F, ref_D, k)
+        assert sloss[l] == pytest.approx(ref_s, rel=1e-6), (l, sloss[l], ref_s)
+        tok = np.sort(rng.choice(N, 256, replace=False))
+        # the oracle's 1/(n^2 k) for n sampled tokens, rescaled to the full N
+        _, ref_g = orc.surrogate(x[tok], F[:, tok], ref_D, k, scale=(len(tok) / N) ** 2)
+        got_g = grad[l][torch.from_numpy(tok).cuda()].cpu().numpy().astype(np.float64)
+        tol = 1e-5 * np.abs(ref_g) + 1e-6 * np.abs(ref_g).max()
+        assert (np.abs(got_g - ref_g) <= tol).all(), f"layer {l}: sampled gradients differ"
+        del x, F
 
 
 def test_more_than_2_31_tokens(dl, orc):

@@ -130,3 +130,37 @@ def test_stream_reset_append_finalize_replays_from_a_graph(dl, syn, E, k):
         assert torch.equal(out, ref_out), f"replay {rep}: loss records differ"
         del y
     s.close()
+
+
+def test_capture_while_the_schedule_tuner_is_measuring(dl, syn):
+    # 4,194,304 tokens = 8,192 work units: the run-time schedule choice
+    # applies.  The first eager call of the shape is unmeasured and the second
+    # leaves a measured trial pending, so the capture happens while the tuner
+    # is mid-way; a captured launch must not touch the measurement events and
+    # must replay to the eager result, and eager calls after the capture
+    # (which finish the measurement) must agree too.
+    E, k, N = 16, 2, 1 << 22
+    print(f"[case] graph during tuning E={E} k={k} N={N}", flush=True)
+    xd = to_dev(syn.normal(909, N, E, 1))
+    ref = dl.do_fused(xd, k, want_bits=True)
+    torch.cuda.synchronize()
+    again = dl.do_fused(xd, k, want_bits=True)  # a measured trial
+    bits = torch.zeros_like(ref[0])
+    D = torch.zeros_like(ref[1])
+    out = torch.zeros_like(ref[2])
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        dl.do_fused(xd, k, bits=bits, D=D, out=out)
+    torch.cuda.synchronize()
+    assert all(torch.equal(a, b) for a, b in zip(again, ref)), "second eager call differs"
+    for rep in range(3):
+        bits.zero_()
+        D.fill_(-1)
+        out.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(bits, ref[0]) and torch.equal(D, ref[1]) and torch.equal(out, ref[2]), rep
+        more = dl.do_fused(xd, k, want_bits=True)  # eager calls complete the measurement
+        torch.cuda.synchronize()
+        assert all(torch.equal(a, b) for a, b in zip(more, ref)), f"eager call {rep} after capture differs"

@@ -233,6 +233,30 @@ def test_loss_of_arbitrary_matrices(dl):
         assert rec["sum"] == int(v.sum()) and rec["sumsq"] == int((v * v).sum()), f"E={E}"
 
 
+@pytest.mark.parametrize("E,hi", [(2, (1 << 32) - 1), (64, (1 << 32) - 1), (300, 3_000_000_000), (1024, (1 << 32) - 1),
+                                  (5, 1 << 30)])
+def test_loss_of_matrices_with_entries_near_2_32(dl, E, hi):
+    # Any uint32 entries: the sum of squares is exact in 128 bits, `sumsq`
+    # saturates at 2^64 - 1 once it does not fit, `loss` is the exact sum in
+    # fp64 and `var` the exact population variance, both pinned here with
+    # Python integers (E = 5 with entries < 2^30 stays below 2^64: exact sumsq).
+    rng = np.random.default_rng(E)
+    D = rng.integers(hi // 2, hi, size=(2, E, E), dtype=np.uint64).astype(np.uint32)
+    D[1, 0, 1 % E] = hi  # the largest entry, once
+    out = dl.do_loss(torch.from_numpy(D.view(np.int32)).cuda())
+    torch.cuda.synchronize()
+    for l, rec in enumerate(dl.loss_records(out)):
+        v = [int(a) for a in D[l][~np.eye(E, dtype=bool)]]
+        P = E * (E - 1)
+        s1, s2 = sum(v), sum(a * a for a in v)
+        assert rec["sum"] == s1
+        assert rec["sumsq"] == (s2 if s2 < (1 << 64) else (1 << 64) - 1), (E, s2)
+        assert rec["loss"] == pytest.approx(float(s2), rel=4.5e-16)
+        assert rec["mean"] == pytest.approx(s1 / P, rel=1e-15)
+        var = (s2 * P - s1 * s1) / (P * P)  # exact rational, rounded once
+        assert rec["var"] == pytest.approx(var, rel=1e-12)
+
+
 def test_hamming_of_oracle_signatures(dl, orc, syn):
     x = syn.normal(12, 5000, 96, 1)
     F = orc.topk_signature(x, 7)

@@ -196,3 +196,37 @@ def test_planted_surrogate_mistake_is_caught(syn, orc, tmp_path, name):
     src = open(SRC).read()
     assert old in src, name
     assert not _pins_hold(_variant(tmp_path, name, src.replace(old, new)), syn, orc), f"mutant {name} survived"
+
+
+# ---------------------------------------------------------------------------
+# surrogate_loss_blocked: the same Eq. (7) loss with the token sums of C taken
+# by a matrix product over token blocks.  Pinned to the pins above: the worked
+# E=2 example, the closed form at unit distances, and the looped oracle on
+# random inputs (fp32 and bf16 p, blocks that split the tokens unevenly).
+# ---------------------------------------------------------------------------
+def test_blocked_loss_worked_example(orc):
+    p = np.array([[0.75, 0.25], [0.5, 0.5]], np.float32)
+    F = np.array([[1, 0], [0, 1]], np.uint8)
+    G = np.array([[0, 2], [2, 0]], np.uint32)
+    assert orc.surrogate_loss_blocked(p, F, G, 1, block=1) == pytest.approx(2 * (0.75 - 0.5 - 0.25 + 0.5) / 4,
+                                                                           rel=1e-15)
+
+
+def test_blocked_loss_closed_form_with_unit_distances(syn, orc):
+    N, E, k = 120, 10, 3
+    p, F, _ = _setup(syn, orc, 31, N, E, k)
+    G = np.ones((E, E), np.uint32) - np.eye(E, dtype=np.uint32)
+    pd = p.astype(np.float64)
+    sK = (pd * F.T.astype(np.float64)).sum(axis=1)
+    expect = (E * sK - k * pd.sum(axis=1)).sum() / (N * N * k)
+    assert orc.surrogate_loss_blocked(p, F, G, k, block=37) == pytest.approx(expect, rel=1e-12, abs=1e-15)
+
+
+@pytest.mark.parametrize("N,E,k,bf16,block", [(500, 16, 4, False, 64), (333, 24, 3, True, 100),
+                                              (1000, 8, 2, False, 1 << 18)])
+def test_blocked_loss_matches_the_looped_oracle(syn, orc, N, E, k, bf16, block):
+    p, F, D = _setup(syn, orc, 61 + E, N, E, k)
+    if bf16:
+        p = (p.view(np.uint32) >> 16).astype(np.uint16)  # truncated bf16 patterns of the probabilities
+    L, _ = orc.surrogate(p, F, D, k, scale=0.5, want_grad=False)
+    assert orc.surrogate_loss_blocked(p, F, D, k, scale=0.5, block=block) == pytest.approx(L, rel=1e-11)
