@@ -233,6 +233,77 @@ int64_t do_stream_words_per_expert(const do_stream* h);
 do_status do_profile_next(hipEvent_t start, hipEvent_t stop);
 
 /*
+ * Replica Expert Mechanism (REM) scheduling on the device.  One replica
+ * placement (Alg. 1) or one token route (Alg. 2): `tokens` tokens of expert
+ * `expert` go from its home rank `src_rank` to its replica on `dst_rank`
+ * (24 bytes).
+ */
+typedef struct {
+  int32_t expert;
+  int32_t src_rank;
+  int32_t dst_rank;
+  int32_t reserved; /* 0 */
+  int64_t tokens;
+} do_rem_move;
+
+/*
+ * REM global-batch replica allocation (Sec. 3.2.1, Benefit Score; App. B,
+ * Alg. 1), one independent problem per layer.  With tau the mean rank load,
+ * the Benefit Score of expert e (home rank r_s) for a replica on r_r is
+ *   min(tau - L_r, T_e, L_s - tau)      if L_r < tau < L_s
+ *   min(floor((L_s - L_r) / 2), T_e)    if L_r >= tau and L_s > L_r
+ *   -1                                  otherwise,
+ * the two differences with tau rounded down to whole tokens.  While some rank
+ * has fewer than D replicas, the least-loaded such rank (lowest index on
+ * ties) receives a replica of the expert with the largest score among the
+ * experts homed elsewhere (lowest expert index on ties), and L_r, L_s and T_e
+ * move by that score; a largest score <= 0 stops the allocation.
+ *   rank_load      nullable, [L][R] device: historical loads L_r; NULL takes
+ *                  L_r = sum of expert_tokens over the experts homed on r
+ *   expert_tokens  [L][E] device: volumes T_e (e.g. the loads of do_load_stats)
+ *   expert_rank    HOST array [E] of home ranks in [0, R), read during the call
+ *   moves          [L][R*D] device: the first n_moves[l] entries of layer l
+ *                  are the placements in order
+ *   n_moves        [L] device; -1 when a load or volume of layer l is negative
+ *                  or >= 2^40 (then nothing else of that layer is written)
+ *   load_out       nullable, [L][R] device: L_r after the last placement
+ *   tokens_out     nullable, [L][E] device: T_e after the last placement
+ * Limits: 1 <= E <= 1024, 1 <= R <= 1024, D >= 1 with R*D <= 4096,
+ * 1 <= L <= 65535.  Integer results are exact and deterministic.
+ */
+do_status do_rem_allocate(const int64_t* rank_load, const int64_t* expert_tokens, const int32_t* expert_rank,
+                          int32_t E, int32_t R, int32_t D, int32_t L, do_rem_move* moves, int32_t* n_moves,
+                          int64_t* load_out, int64_t* tokens_out, hipStream_t stream);
+
+/*
+ * REM micro-batch token dispatching (App. B, Alg. 2), one problem per layer.
+ * The queue depth Q_r starts as the sum of this micro-batch's volumes T_e
+ * over the experts homed on r; tau is their mean.  D passes: each orders the
+ * ranks by Q_r ascending (ties by index, no re-sorting within the pass) and,
+ * for every rank holding a replica, routes the Benefit Score's number of
+ * tokens (with L = Q) through the best of its replicas (earliest in the
+ * assignment on ties); a score <= 0 routes nothing.
+ *   replicas       [L][replica_stride] device: the assignment, e.g. the moves
+ *                  of do_rem_allocate (expert, src_rank = its home rank,
+ *                  dst_rank = the replica's rank; `tokens` is ignored)
+ *   n_replicas     [L] device: valid entries per layer (a negative count, or
+ *                  a replica whose src_rank is not its expert's home rank,
+ *                  fails the layer as below)
+ *   expert_tokens  [L][E] device: this micro-batch's volumes T_e
+ *   expert_rank    HOST array [E] of home ranks in [0, R), read during the call
+ *   routes         [L][R*D] device: the first n_routes[l] entries are the routes
+ *   n_routes       [L] device; -1 for invalid input of layer l (volumes outside
+ *                  [0, 2^40), a bad replica or count)
+ *   queue_out      nullable, [L][R] device: Q_r after the last pass
+ *   tokens_out     nullable, [L][E] device: T_e after the last pass
+ * Limits: as do_rem_allocate, and replica_stride <= 4096.
+ */
+do_status do_rem_dispatch(const do_rem_move* replicas, const int32_t* n_replicas, int32_t replica_stride,
+                          const int64_t* expert_tokens, const int32_t* expert_rank, int32_t E, int32_t R, int32_t D,
+                          int32_t L, do_rem_move* routes, int32_t* n_routes, int64_t* queue_out, int64_t* tokens_out,
+                          hipStream_t stream);
+
+/*
  * Process-wide overrides of internal choices that never change any result,
  * for tests and benchmarks (they take effect at the next call; calls already
  * enqueued are unaffected).  Returns DO_ERR_INVALID_ARG for an unknown option

@@ -13,6 +13,7 @@ Functions keep the C names:
 * ``do_fused(scores, k, want_bits)`` -> (bits or None, D, out)
 * ``do_surrogate(p, k, bits, D)``    -> (loss [L] float64, dloss/dp [L][N][E] float32)
 * ``DoStream``                       -> streaming history (do_stream_*)
+* ``do_rem_allocate`` / ``do_rem_dispatch`` -> REM replica placement and token routes
 
 ``scores`` is a CUDA tensor of shape [N, E] or [L, N, E], float32 or bfloat16.
 """
@@ -73,6 +74,8 @@ def lib():
             "do_version": ([], i32),
             "do_profile_next": ([vp, vp], st),
             "do_set_option": ([st, i32], st),
+            "do_rem_allocate": ([vp, vp, vp, i32, i32, i32, i32, vp, vp, vp, vp, vp], st),
+            "do_rem_dispatch": ([vp, vp, i32, vp, vp, i32, i32, i32, i32, vp, vp, vp, vp, vp], st),
         }
         for name, (args, res) in sigs.items():
             f = getattr(L, name)
@@ -327,6 +330,84 @@ def do_profile_next(start: "torch.cuda.Event | None", stop: "torch.cuda.Event | 
     a = ctypes.c_void_p(start.cuda_event) if start is not None else None
     b = ctypes.c_void_p(stop.cuda_event) if stop is not None else None
     _check(lib().do_profile_next(a, b), "do_profile_next")
+
+
+REM_MOVE_WORDS = 3  # do_rem_move: 24 bytes = 3 int64 words
+
+
+def _rank_array(expert_rank, E: int):
+    if expert_rank is None or len(expert_rank) != E:
+        raise ValueError(f"expert_rank must list the home rank of each of the E = {E} experts")
+    return (ctypes.c_int32 * E)(*[int(r) for r in expert_rank])
+
+
+def do_rem_allocate(expert_tokens: torch.Tensor, expert_rank, R: int, D: int, rank_load: torch.Tensor | None = None,
+                    want_state: bool = True):
+    """REM Alg. 1 per layer.  expert_tokens: int64 [L, E] (or [E]); expert_rank: host
+    sequence of E home ranks; rank_load: int64 [L, R] or None (sum of the volumes).
+    Returns (moves int64 [L, R*D, 3] (see rem_records), n_moves int32 [L],
+    load_out int64 [L, R] or None, tokens_out int64 [L, E] or None)."""
+    if not isinstance(expert_tokens, torch.Tensor) or expert_tokens.dim() not in (1, 2):
+        raise ValueError("expert_tokens must be a tensor of shape [E] or [L, E]")
+    T = expert_tokens if expert_tokens.dim() == 2 else expert_tokens.unsqueeze(0)
+    L, E = T.shape
+    _want(T, "expert_tokens", dtypes=_I64)
+    if rank_load is not None:
+        rank_load = rank_load if rank_load.dim() == 2 else rank_load.unsqueeze(0)
+        _want(rank_load, "rank_load", shape=(L, R), dtypes=_I64)
+    rk = _rank_array(expert_rank, E)
+    dev = T.device
+    moves = torch.zeros((L, R * D, REM_MOVE_WORDS), dtype=torch.int64, device=dev)
+    n = torch.empty(L, dtype=torch.int32, device=dev)
+    lo = torch.empty((L, R), dtype=torch.int64, device=dev) if want_state else None
+    to = torch.empty((L, E), dtype=torch.int64, device=dev) if want_state else None
+    _check(lib().do_rem_allocate(rank_load.data_ptr() if rank_load is not None else None, T.data_ptr(), rk, E, R, D,
+                                 L, moves.data_ptr(), n.data_ptr(), lo.data_ptr() if lo is not None else None,
+                                 to.data_ptr() if to is not None else None, _stream()), "do_rem_allocate")
+    return moves, n, lo, to
+
+
+def do_rem_dispatch(replicas: torch.Tensor, n_replicas: torch.Tensor, expert_tokens: torch.Tensor, expert_rank,
+                    R: int, D: int, want_state: bool = True):
+    """REM Alg. 2 per layer.  replicas: int64 [L, S, 3] assignment records (e.g. the
+    moves of do_rem_allocate) with n_replicas int32 [L] valid each; expert_tokens:
+    int64 [L, E] volumes of this micro-batch.  Returns (routes int64 [L, R*D, 3],
+    n_routes int32 [L], queue_out int64 [L, R] or None, tokens_out int64 [L, E] or None)."""
+    if not isinstance(replicas, torch.Tensor) or replicas.dim() != 3 or replicas.shape[2] != REM_MOVE_WORDS:
+        raise ValueError("replicas must be a tensor of shape [L, S, 3]")
+    L, S = replicas.shape[0], replicas.shape[1]
+    _want(replicas, "replicas", dtypes=_I64)
+    _want(n_replicas, "n_replicas", shape=(L,), dtypes=_I32)
+    T = expert_tokens if expert_tokens.dim() == 2 else expert_tokens.unsqueeze(0)
+    if T.shape[0] != L:
+        raise ValueError(f"expert_tokens has {T.shape[0]} layers, replicas {L}")
+    E = T.shape[1]
+    _want(T, "expert_tokens", dtypes=_I64)
+    rk = _rank_array(expert_rank, E)
+    dev = T.device
+    routes = torch.zeros((L, R * D, REM_MOVE_WORDS), dtype=torch.int64, device=dev)
+    n = torch.empty(L, dtype=torch.int32, device=dev)
+    qo = torch.empty((L, R), dtype=torch.int64, device=dev) if want_state else None
+    to = torch.empty((L, E), dtype=torch.int64, device=dev) if want_state else None
+    _check(lib().do_rem_dispatch(replicas.data_ptr(), n_replicas.data_ptr(), S, T.data_ptr(), rk, E, R, D, L,
+                                 routes.data_ptr(), n.data_ptr(), qo.data_ptr() if qo is not None else None,
+                                 to.data_ptr() if to is not None else None, _stream()), "do_rem_dispatch")
+    return routes, n, qo, to
+
+
+def rem_records(moves: torch.Tensor, n: torch.Tensor) -> list:
+    """Decode do_rem_move records: per layer a list of (expert, src_rank, dst_rank, tokens),
+    or None for a layer whose count is -1 (invalid input)."""
+    m = moves.detach().cpu().contiguous().numpy()
+    cnt = n.detach().cpu().numpy()
+    out = []
+    for l in range(m.shape[0]):
+        if cnt[l] < 0:
+            out.append(None)
+            continue
+        w = m[l, :cnt[l]]
+        out.append([(int(a) & 0xFFFFFFFF, (int(a) >> 32) & 0xFFFFFFFF, int(b) & 0xFFFFFFFF, int(c)) for a, b, c in w])
+    return out
 
 
 class DoStream:

@@ -272,6 +272,69 @@ DOLOSS_API do_status do_load_stats(const uint64_t* bits, int64_t N, int64_t ld, 
                     "load stats");
 }
 
+namespace {
+
+// Shared checks of the REM entry points; fills the home-rank map.
+do_status check_rem(const int32_t* expert_rank, int32_t E, int32_t R, int32_t D, int32_t L, dol::RankMap& rm) {
+  if (E < 1 || E > dol::kMaxE) return fail(DO_ERR_INVALID_ARG, "E must be in [1, 1024]");
+  if (R < 1 || R > dol::kMaxE) return fail(DO_ERR_INVALID_ARG, "R must be in [1, 1024]");
+  if (D < 1 || (int64_t)R * D > 4096) return fail(DO_ERR_INVALID_ARG, "D must be >= 1 with R*D <= 4096");
+  if (L < 1 || L > 65535) return fail(DO_ERR_INVALID_ARG, "L must be in [1, 65535]");
+  if (expert_rank == nullptr) return fail(DO_ERR_INVALID_ARG, "expert_rank is NULL");
+  for (int32_t i = 0; i < E; ++i) {
+    if (expert_rank[i] < 0 || expert_rank[i] >= R)
+      return fail(DO_ERR_INVALID_ARG, "expert_rank[" + std::to_string(i) + "] is not in [0, R)");
+    rm.rank[i] = (uint16_t)expert_rank[i];
+  }
+  rm.R = R;
+  rm.given = 1;
+  return DO_OK;
+}
+
+}  // namespace
+
+DOLOSS_API do_status do_rem_allocate(const int64_t* rank_load, const int64_t* expert_tokens,
+                                     const int32_t* expert_rank, int32_t E, int32_t R, int32_t D, int32_t L,
+                                     do_rem_move* moves, int32_t* n_moves, int64_t* load_out, int64_t* tokens_out,
+                                     hipStream_t stream) {
+  dol::RankMap rm{};
+  DO_TRY(check_rem(expert_rank, E, R, D, L, rm));
+  if (rank_load != nullptr && !aligned(rank_load, 8)) return fail(DO_ERR_INVALID_ARG, "rank_load is not 8-byte aligned");
+  if (expert_tokens == nullptr || !aligned(expert_tokens, 8))
+    return fail(DO_ERR_INVALID_ARG, "expert_tokens is NULL or not 8-byte aligned");
+  if (moves == nullptr || !aligned(moves, 8)) return fail(DO_ERR_INVALID_ARG, "moves is NULL or not 8-byte aligned");
+  if (n_moves == nullptr || !aligned(n_moves, 4)) return fail(DO_ERR_INVALID_ARG, "n_moves is NULL or not 4-byte aligned");
+  if ((load_out != nullptr && !aligned(load_out, 8)) || (tokens_out != nullptr && !aligned(tokens_out, 8)))
+    return fail(DO_ERR_INVALID_ARG, "load_out / tokens_out is not 8-byte aligned");
+  return hip_status(dol::launch_rem_allocate(rank_load, expert_tokens, rm, E, D, L, moves, n_moves, load_out,
+                                             tokens_out, stream),
+                    "rem allocate");
+}
+
+DOLOSS_API do_status do_rem_dispatch(const do_rem_move* replicas, const int32_t* n_replicas, int32_t replica_stride,
+                                     const int64_t* expert_tokens, const int32_t* expert_rank, int32_t E, int32_t R,
+                                     int32_t D, int32_t L, do_rem_move* routes, int32_t* n_routes, int64_t* queue_out,
+                                     int64_t* tokens_out, hipStream_t stream) {
+  dol::RankMap rm{};
+  DO_TRY(check_rem(expert_rank, E, R, D, L, rm));
+  if (replica_stride < 1 || replica_stride > 4096)
+    return fail(DO_ERR_INVALID_ARG, "replica_stride must be in [1, 4096]");
+  if (replicas == nullptr || !aligned(replicas, 8))
+    return fail(DO_ERR_INVALID_ARG, "replicas is NULL or not 8-byte aligned");
+  if (n_replicas == nullptr || !aligned(n_replicas, 4))
+    return fail(DO_ERR_INVALID_ARG, "n_replicas is NULL or not 4-byte aligned");
+  if (expert_tokens == nullptr || !aligned(expert_tokens, 8))
+    return fail(DO_ERR_INVALID_ARG, "expert_tokens is NULL or not 8-byte aligned");
+  if (routes == nullptr || !aligned(routes, 8)) return fail(DO_ERR_INVALID_ARG, "routes is NULL or not 8-byte aligned");
+  if (n_routes == nullptr || !aligned(n_routes, 4))
+    return fail(DO_ERR_INVALID_ARG, "n_routes is NULL or not 4-byte aligned");
+  if ((queue_out != nullptr && !aligned(queue_out, 8)) || (tokens_out != nullptr && !aligned(tokens_out, 8)))
+    return fail(DO_ERR_INVALID_ARG, "queue_out / tokens_out is not 8-byte aligned");
+  return hip_status(dol::launch_rem_dispatch(replicas, n_replicas, replica_stride, expert_tokens, rm, E, D, L, routes,
+                                             n_routes, queue_out, tokens_out, stream),
+                    "rem dispatch");
+}
+
 DOLOSS_API do_status do_stream_create(int32_t E, int32_t k, int64_t capacity_tokens, do_stream** out) {
   if (out == nullptr) return fail(DO_ERR_INVALID_ARG, "out is NULL");
   *out = nullptr;

@@ -112,6 +112,16 @@ hipError_t launch_load_stats(const u64* bits, int64_t N, int64_t ld, int32_t E, 
                              do_dtype dt, const RankMap& rm, uint32_t* loads, do_load_stats_result* out,
                              hipStream_t s);
 
+// REM scheduling (one wavefront per layer); the rank map gives the home
+// ranks (rm.R ranks, rm.given set).
+hipError_t launch_rem_allocate(const int64_t* rank_load, const int64_t* tokens, const RankMap& rm, int32_t E,
+                               int32_t D, int32_t L, do_rem_move* moves, int32_t* n_moves, int64_t* load_out,
+                               int64_t* tokens_out, hipStream_t s);
+hipError_t launch_rem_dispatch(const do_rem_move* replicas, const int32_t* n_rep, int32_t rep_stride,
+                               const int64_t* tokens, const RankMap& rm, int32_t E, int32_t D, int32_t L,
+                               do_rem_move* routes, int32_t* n_routes, int64_t* queue_out, int64_t* tokens_out,
+                               hipStream_t s);
+
 // Loss of arbitrary distance matrices.
 // One layer (E <= 256) over ceil(E/8) blocks; fin: three u64 that are zero
 // before the call and zero again after it (cacc must not alias D).

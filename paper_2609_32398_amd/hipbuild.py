@@ -7,7 +7,7 @@ import subprocess
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB_PATH = os.path.join(HERE, "libdoloss.so")
-SOURCES = ["api.hip", "topk.hip", "reduce.hip", "surrogate.hip", "loadstats.hip"]
+SOURCES = ["api.hip", "topk.hip", "reduce.hip", "surrogate.hip", "loadstats.hip", "rem.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",

@@ -252,3 +252,40 @@ def test_fused_without_bits_needs_e_at_most_256(dl):
     # is not called here (it would launch)
     assert _st(dl, "do_fused", FAKE, 0, 64, 257, 8, 1, None, FAKE, FAKE, None) == 1
     assert b"bits" in dl.lib().do_last_error()
+
+
+def test_rem_entry_points_reject_bad_arguments(dl):
+    L = dl.lib()
+    ranks = _ranks([0, 1, 1, 0])
+    bad_rank = _ranks([0, 2, 1, 0])
+    ok = (None, FAKE, ranks, 4, 2, 1, 1, FAKE, FAKE, None, None, None)
+    cases = [
+        ((None, None, ranks, 4, 2, 1, 1, FAKE, FAKE, None, None, None), 1),   # NULL expert_tokens
+        ((None, FAKE, None, 4, 2, 1, 1, FAKE, FAKE, None, None, None), 1),    # NULL expert_rank
+        ((None, FAKE, bad_rank, 4, 2, 1, 1, FAKE, FAKE, None, None, None), 1),  # a rank >= R
+        ((None, FAKE, ranks, 0, 2, 1, 1, FAKE, FAKE, None, None, None), 1),   # E = 0
+        ((None, FAKE, ranks, 4, 0, 1, 1, FAKE, FAKE, None, None, None), 1),   # R = 0
+        ((None, FAKE, ranks, 4, 2, 0, 1, FAKE, FAKE, None, None, None), 1),   # D = 0
+        ((None, FAKE, ranks, 4, 2, 2049, 1, FAKE, FAKE, None, None, None), 1),  # R*D > 4096
+        ((None, FAKE, ranks, 4, 2, 1, 0, FAKE, FAKE, None, None, None), 1),   # L = 0
+        ((None, FAKE, ranks, 4, 2, 1, 1, None, FAKE, None, None, None), 1),   # NULL moves
+        ((None, FAKE, ranks, 4, 2, 1, 1, FAKE, None, None, None, None), 1),   # NULL n_moves
+        ((FAKE + 4, FAKE, ranks, 4, 2, 1, 1, FAKE, FAKE, None, None, None), 1),  # misaligned rank_load
+        ((None, FAKE, ranks, 4, 2, 1, 1, FAKE, FAKE, FAKE + 4, None, None), 1),  # misaligned load_out
+    ]
+    assert ok  # the valid argument set is not called (it would launch)
+    for args, expect in cases:
+        assert L.do_rem_allocate(*args) == expect, args
+        assert L.do_last_error()
+    d = [
+        ((None, FAKE, 2, FAKE, ranks, 4, 2, 1, 1, FAKE, FAKE, None, None, None), 1),   # NULL replicas
+        ((FAKE, None, 2, FAKE, ranks, 4, 2, 1, 1, FAKE, FAKE, None, None, None), 1),   # NULL counts
+        ((FAKE, FAKE, 0, FAKE, ranks, 4, 2, 1, 1, FAKE, FAKE, None, None, None), 1),   # stride 0
+        ((FAKE, FAKE, 4097, FAKE, ranks, 4, 2, 1, 1, FAKE, FAKE, None, None, None), 1),  # stride > 4096
+        ((FAKE, FAKE, 2, None, ranks, 4, 2, 1, 1, FAKE, FAKE, None, None, None), 1),   # NULL tokens
+        ((FAKE, FAKE, 2, FAKE, bad_rank, 4, 2, 1, 1, FAKE, FAKE, None, None, None), 1),  # a rank >= R
+        ((FAKE, FAKE, 2, FAKE, ranks, 4, 2, 1, 1, None, FAKE, None, None, None), 1),   # NULL routes
+        ((FAKE, FAKE, 2, FAKE, ranks, 4, 2, 1, 1, FAKE, FAKE, None, FAKE + 4, None), 1),  # misaligned tokens_out
+    ]
+    for args, expect in d:
+        assert L.do_rem_dispatch(*args) == expect, args
