@@ -233,6 +233,30 @@ int64_t do_stream_words_per_expert(const do_stream* h);
 do_status do_profile_next(hipEvent_t start, hipEvent_t stop);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the result
+ * of do_stream_create + do_stream_append_many + do_stream_finalize on one
+ * global batch of `count` micro-batches, in one call that allocates nothing.
+ * The caller owns the history; the running co-occurrence counts and the
+ * finalize's partial sums live in a static device buffer of the library
+ * (256 KiB + 32 bytes, held on every GPU the library runs on until the
+ * process ends), which every call clears before use.
+ *   scores         HOST array of `count` (1..64) device pointers, each
+ *                  [n_tokens_each][E], read during the call
+ *   hist           [E][ceil(count * n_tokens_each / 64)] device: the signatures
+ *                  of the tokens in order (as do_stream_bits), overwritten
+ *   D, out         as do_stream_finalize
+ * Limits: E <= 256 (DO_ERR_INVALID_ARG otherwise), 1 <= k <= E,
+ * n_tokens_each >= 1, count * n_tokens_each < 2^32 and the limits of
+ * do_topk_signature.  All calls on one GPU share the buffer: calls that may
+ * overlap in time (on different streams, or from several threads without
+ * ordering) race and give wrong results.
+ */
+do_status do_global_batch_noalloc(const void* const* scores, do_dtype dtype, int64_t n_tokens_each, int32_t count,
+                                  int32_t E, int32_t k, uint64_t* hist, uint32_t* D, do_loss_result* out,
+                                  hipStream_t stream);
+
+/*
  * Replica Expert Mechanism (REM) scheduling on the device.  One replica
  * placement (Alg. 1) or one token route (Alg. 2): `tokens` tokens of expert
  * `expert` go from its home rank `src_rank` to its replica on `dst_rank`

@@ -74,6 +74,7 @@ def lib():
             "do_version": ([], i32),
             "do_profile_next": ([vp, vp], st),
             "do_set_option": ([st, i32], st),
+            "do_global_batch_noalloc": ([ctypes.POINTER(vp), st, i64, i32, i32, i32, vp, vp, vp, vp], st),
             "do_rem_allocate": ([vp, vp, vp, i32, i32, i32, i32, vp, vp, vp, vp, vp], st),
             "do_rem_dispatch": ([vp, vp, i32, vp, vp, i32, i32, i32, i32, vp, vp, vp, vp, vp], st),
         }
@@ -330,6 +331,37 @@ def do_profile_next(start: "torch.cuda.Event | None", stop: "torch.cuda.Event | 
     a = ctypes.c_void_p(start.cuda_event) if start is not None else None
     b = ctypes.c_void_p(stop.cuda_event) if stop is not None else None
     _check(lib().do_profile_next(a, b), "do_profile_next")
+
+
+def do_global_batch_noalloc(score_list, k: int, hist: torch.Tensor | None = None, D: torch.Tensor | None = None,
+                            out: torch.Tensor | None = None):
+    """do_global_batch_noalloc: the history, distances and loss of one global batch of
+    micro-batches (each [n, E] on the device) in one call that allocates nothing in the
+    library.  Returns (hist int64 [E, ceil(count n / 64)], D int32 [E, E], out [1, 40])."""
+    if not 1 <= len(score_list) <= 64:
+        raise ValueError("do_global_batch_noalloc takes 1 to 64 micro-batches")
+    first = score_list[0]
+    if not isinstance(first, torch.Tensor) or first.dim() != 2:
+        raise ValueError("each micro-batch must be a tensor of shape [n_tokens, E]")
+    n, E = first.shape
+    for i, t in enumerate(score_list):
+        if not isinstance(t, torch.Tensor) or t.shape != first.shape or t.dtype != first.dtype:
+            raise ValueError(f"scores[{i}] differs in shape or dtype from scores[0]")
+        _want(t, f"scores[{i}]", dtypes=_SCORE_DTYPES)
+    W = _words(len(score_list) * n)
+    if hist is None:
+        hist = torch.empty((E, W), dtype=torch.int64, device=first.device)
+    if D is None:
+        D = torch.empty((E, E), dtype=torch.int32, device=first.device)
+    if out is None:
+        out = alloc_out(1, first.device)
+    _want(hist, "hist", numel=E * W, dtypes=_I64)
+    _want(D, "D", numel=E * E, dtypes=_I32)
+    _want(out, "out", numel=LOSS_RESULT_BYTES, dtypes=_U8)
+    ptrs = (ctypes.c_void_p * len(score_list))(*[t.data_ptr() for t in score_list])
+    _check(lib().do_global_batch_noalloc(ptrs, _dtype_code(first), n, len(score_list), E, k, hist.data_ptr(),
+                                         D.data_ptr(), out.data_ptr(), _stream()), "do_global_batch_noalloc")
+    return hist, D, out
 
 
 REM_MOVE_WORDS = 3  # do_rem_move: 24 bytes = 3 int64 words

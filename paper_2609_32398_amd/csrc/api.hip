@@ -1,6 +1,7 @@
 // Host side of the C ABI declared in include/doloss.h: argument validation,
 // dispatch to the kernels, and the streaming-history handles.
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 
@@ -467,3 +468,98 @@ DOLOSS_API const uint64_t* do_stream_bits(const do_stream* h) {
 DOLOSS_API int64_t do_stream_tokens(const do_stream* h) { return h ? h->tokens : -1; }
 
 DOLOSS_API int64_t do_stream_words_per_expert(const do_stream* h) { return h ? h->W : -1; }
+
+// ---------------------------------------------------------------------------
+// Global batch without any allocation (do_global_batch_noalloc).  The running
+// co-occurrence counts and the split finalize's two sums and ticket live in a
+// file-scope device array instead of a handle's allocation.  Its address is
+// looked up once per device with hipGetSymbolAddress (in host code the
+// array's name is not a device address) and only that pointer is used.
+// ---------------------------------------------------------------------------
+namespace {
+
+constexpr int32_t kNoAllocMaxE = dol::kFastMaxE;                                  // 256 experts
+constexpr int64_t kNoAllocCountWords = (int64_t)kNoAllocMaxE * kNoAllocMaxE / 2;  // E*E uint32 counters
+constexpr int64_t kNoAllocWords = kNoAllocCountWords + 4;                         // + sums, ticket, pad
+constexpr int kMaxDevices = 64;
+
+}  // namespace
+
+static __device__ __align__(256) u64 scratch[kNoAllocWords];  // 256 KiB + 32 B on every device
+
+namespace {
+
+std::mutex g_scratch_mu;
+u64* g_scratch_ptr[kMaxDevices] = {};
+
+// The device address of `scratch` on the current device (looked up on the
+// first call on that device).
+do_status scratch_on_device(u64** out) {
+  int dev = -1;
+  DO_TRY(hip_status(hipGetDevice(&dev), "hipGetDevice"));
+  if (dev < 0 || dev >= kMaxDevices) return fail(DO_ERR_INVALID_ARG, "device index beyond 63");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    DO_TRY(hip_status(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)"));
+    if (p == nullptr) return fail(DO_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[dev] = static_cast<u64*>(p);
+  }
+  *out = g_scratch_ptr[dev];
+  return DO_OK;
+}
+
+}  // namespace
+
+DOLOSS_API do_status do_global_batch_noalloc(const void* const* scores, do_dtype dtype, int64_t n_tokens_each,
+                                             int32_t count, int32_t E, int32_t k, uint64_t* hist, uint32_t* D,
+                                             do_loss_result* out, hipStream_t stream) {
+  DO_TRY(check_dtype(dtype));
+  if (E > kNoAllocMaxE)
+    return fail(DO_ERR_INVALID_ARG, "do_global_batch_noalloc supports E <= 256 (its static counters hold 256 x 256)");
+  if (count < 1 || count > dol::kMaxSeg) return fail(DO_ERR_INVALID_ARG, "count must be in [1, 64]");
+  if (n_tokens_each < 1) return fail(DO_ERR_INVALID_ARG, "n_tokens_each must be >= 1");
+  if (n_tokens_each > ((int64_t(1) << 32) - 1) / count)
+    return fail(DO_ERR_OVERFLOW, "count * n_tokens_each must be < 2^32 (distances are uint32)");
+  const int64_t N = (int64_t)count * n_tokens_each;
+  DO_TRY(check_shape(N, E, 1));
+  DO_TRY(check_k(k, E));
+  if (scores == nullptr) return fail(DO_ERR_INVALID_ARG, "scores pointer array is NULL");
+  bool fast = true;
+  for (int i = 0; i < count; ++i) {
+    DO_TRY(check_scores(scores[i], dtype));
+    fast = fast && fast_layout(scores[i], dtype, E);
+  }
+  if (hist == nullptr || !aligned(hist, 8)) return fail(DO_ERR_INVALID_ARG, "hist is NULL or not 8-byte aligned");
+  if (D == nullptr || !aligned(D, 4)) return fail(DO_ERR_INVALID_ARG, "D is NULL or not 4-byte aligned");
+  if (out == nullptr || !aligned(out, 8)) return fail(DO_ERR_INVALID_ARG, "out is NULL or not 8-byte aligned");
+  u64* sp = nullptr;
+  DO_TRY(scratch_on_device(&sp));
+  uint32_t* cacc = reinterpret_cast<uint32_t*>(sp);
+  u64* fin = sp + kNoAllocCountWords;
+  const int64_t W = (N + 63) / 64;
+  // every word the appends OR into starts at zero, and so do the counts and
+  // the finalize's sums (fill kernels: no memset nodes under graph capture)
+  DO_TRY(hip_status(dol::launch_fill_u64(reinterpret_cast<u64*>(hist), (int64_t)E * W, stream), "fill history"));
+  DO_TRY(hip_status(dol::launch_fill_u64(sp, ((int64_t)E * E + 1) / 2, stream), "fill counters"));
+  DO_TRY(hip_status(dol::launch_fill_u64(fin, 3, stream), "fill finalize words"));
+  dol::PathArgs a{};
+  a.E = E;
+  a.k = k;
+  a.bits = reinterpret_cast<u64*>(hist);
+  a.bits_layer_words = (int64_t)E * W;
+  a.W = W;
+  a.or_partial = 1;
+  a.cacc = cacc;
+  a.cacc_layer_elems = (int64_t)E * E;
+  dol::SegTable tab{};
+  for (int i = 0; i < count; ++i) {
+    tab.s[i].scores = scores[i];
+    tab.s[i].n = n_tokens_each;
+    tab.s[i].tok_off = (int64_t)i * n_tokens_each;
+    tab.s[i].layer = 0;
+  }
+  DO_TRY(hip_status(profiled(stream, [&] { return dol::launch_topk(dtype, tab, count, a, fast, stream); }),
+                    "global batch"));
+  return hip_status(dol::launch_finalize_split(cacc, D, out, E, fin, stream), "finalize");
+}

@@ -31,7 +31,7 @@ def test_header_declares_the_path(dl):
     names = _declared()
     for must in ("do_topk_signature", "do_pairwise_hamming", "do_loss", "do_fused", "do_stream_create",
                  "do_stream_append", "do_stream_append_many", "do_stream_finalize", "do_surrogate",
-                 "do_load_stats"):
+                 "do_load_stats", "do_global_batch_noalloc"):
         assert must in names
 
 
@@ -289,3 +289,17 @@ def test_rem_entry_points_reject_bad_arguments(dl):
     ]
     for args, expect in d:
         assert L.do_rem_dispatch(*args) == expect, args
+
+
+def test_noalloc_global_batch_rejects_beyond_its_static_buffer(dl):
+    # the static counters hold 256 x 256: E = 257 is refused on the host with a
+    # clear message, before the device is touched
+    L = dl.lib()
+    ptrs = (ctypes.c_void_p * 2)(FAKE, FAKE)
+    assert L.do_global_batch_noalloc(ptrs, 0, 100, 2, 257, 8, FAKE, FAKE, FAKE, None) == 1
+    assert b"E <= 256" in L.do_last_error()
+    assert L.do_global_batch_noalloc(ptrs, 0, 100, 65, 8, 2, FAKE, FAKE, FAKE, None) == 1   # count > 64
+    assert L.do_global_batch_noalloc(ptrs, 0, 0, 2, 8, 2, FAKE, FAKE, FAKE, None) == 1     # no tokens
+    assert L.do_global_batch_noalloc(ptrs, 0, 1 << 31, 2, 8, 2, FAKE, FAKE, FAKE, None) == 4  # 2^32 tokens
+    assert L.do_global_batch_noalloc(ptrs, 0, 100, 2, 8, 2, None, FAKE, FAKE, None) == 1   # NULL history
+    assert L.do_global_batch_noalloc(None, 0, 100, 2, 8, 2, FAKE, FAKE, FAKE, None) == 1   # NULL pointer array
