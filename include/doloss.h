@@ -205,20 +205,28 @@ do_status do_stream_append_many(do_stream* h, const void* const* scores, do_dtyp
                                 int32_t count, hipStream_t stream);
 
 /* Writes the distances D [E][E] and the loss `out` [1] (both device) of all
- * tokens appended so far.  The history and the counts are not modified.  Calls
- * on one handle must not overlap in time (use one stream, or synchronise):
- * the finalize keeps its partial sums in the handle between its blocks. */
+ * tokens appended so far (since the last reset).  The history is not
+ * modified, and a repeated finalize gives the same result.  Calls on one
+ * handle must not overlap in time (use one stream, or synchronise): the
+ * handle's counters are moved into its running totals here. */
 do_status do_stream_finalize(do_stream* h, uint32_t* D, do_loss_result* out, hipStream_t stream);
 
-/* Clears the history and the counters (enqueued on `stream`). */
+/* Empties the history: the next append starts at token 0 and the next
+ * finalize counts only tokens appended after the reset.  Bits of earlier
+ * tokens are not erased here: the next appends overwrite or clear the words
+ * they use (see do_stream_bits).  Enqueues at most one small fill, and none
+ * when the previous call on the handle was a finalize. */
 do_status do_stream_reset(do_stream* h, hipStream_t stream);
 
 /* Frees the handle after synchronising the device it was created on (the
  * current device is restored).  NULL is accepted. */
 do_status do_stream_destroy(do_stream* h);
 
-/* Device pointer to the history [E][do_stream_words_per_expert(h)]; bits past
- * do_stream_tokens(h) are zero. */
+/* Device pointer to the history [E][do_stream_words_per_expert(h)].  Words
+ * 0 .. ceil(do_stream_tokens(h) / 64) - 1 of every row hold the signatures of
+ * the appended tokens, with zero bits past the last token; words after them
+ * are zero until the first reset and unspecified after it (they may keep bits
+ * of tokens appended before the reset). */
 const uint64_t* do_stream_bits(const do_stream* h);
 int64_t do_stream_tokens(const do_stream* h);
 int64_t do_stream_words_per_expert(const do_stream* h);

@@ -1,5 +1,6 @@
 // Host side of the C ABI declared in include/doloss.h: argument validation,
 // dispatch to the kernels, and the streaming-history handles.
+#include <algorithm>
 #include <cstring>
 #include <mutex>
 #include <new>
@@ -115,6 +116,12 @@ do_status run_layers(const void* scores, do_dtype dt, int64_t N, int32_t E, int3
 
 }  // namespace
 
+// Copies of a stream's co-occurrence counters (block b of an append adds its
+// counts into copy b % kStreamCopies).  Eight copies, one per XCD, were
+// measured: the append kernel took the same time at workload 3 and the
+// finalize, which reads every copy, took longer, so one copy is kept.
+constexpr int32_t kStreamCopies = 1;
+
 struct do_stream_s {
   int32_t E;
   int32_t k;
@@ -122,10 +129,18 @@ struct do_stream_s {
   int64_t W;
   int64_t tokens;
   u64* hist;        // [E][W], at the start of one allocation
-  uint32_t* cacc;   // [E][E], right after the history in the same allocation
-  u64* fin;         // 3 words after the counters: the split finalize's sums and ticket
-  int64_t words;    // u64 words of the allocation (history, counters, finalize words)
+  uint32_t* cacc;   // kStreamCopies x [E][E] counters, after the history
+  uint32_t* snap;   // [E][E]: the totals of the last finalize
+  u64* fin;         // 3 words: the finalize's two sums and its ticket
+  int64_t words;    // u64 words of the allocation
   int device;
+  // Host-side state (the device work it describes is ordered on the caller's
+  // stream): the counter copies hold nothing since the last finalize or
+  // clear; snap holds totals of this epoch (since the last reset); history
+  // words [0, hist_dirty) may hold bits, of this epoch or of earlier ones.
+  bool copies_clean;
+  bool snap_valid;
+  int64_t hist_dirty;
 };
 
 DOLOSS_API const char* do_status_string(do_status s) {
@@ -175,7 +190,7 @@ DOLOSS_API do_status do_pairwise_hamming(const uint64_t* bits, int64_t N, int32_
   if (E <= dol::kFastMaxE && dol::gram_mfma_enabled())
     DO_TRY(hip_status(dol::launch_gram_mfma(reinterpret_cast<const u64*>(bits), W, E, L, D, stream), "gram"));
   else
-    DO_TRY(hip_status(dol::launch_gram_bits(reinterpret_cast<const u64*>(bits), W, E, L, D, stream), "gram"));
+    DO_TRY(hip_status(dol::launch_gram_bits(reinterpret_cast<const u64*>(bits), W, W, E, L, D, stream), "gram"));
   return hip_status(dol::launch_finalize(D, D, nullptr, E, L, stream), "finalize");
 }
 
@@ -202,8 +217,9 @@ DOLOSS_API do_status do_fused(const void* scores, do_dtype dtype, int64_t N, int
     DO_TRY(run_layers(scores, dtype, N, E, k, L, reinterpret_cast<u64*>(bits), D, stream));
   } else {
     DO_TRY(run_layers(scores, dtype, N, E, k, L, reinterpret_cast<u64*>(bits), nullptr, stream));
-    DO_TRY(hip_status(dol::launch_gram_bits(reinterpret_cast<const u64*>(bits), (N + 63) / 64, E, L, D, stream),
-                      "gram"));
+    DO_TRY(hip_status(
+        dol::launch_gram_bits(reinterpret_cast<const u64*>(bits), (N + 63) / 64, (N + 63) / 64, E, L, D, stream),
+        "gram"));
   }
   return hip_status(dol::launch_finalize(D, D, out, E, L, stream), "finalize");
 }
@@ -348,13 +364,19 @@ DOLOSS_API do_status do_stream_create(int32_t E, int32_t k, int64_t capacity_tok
   h->capacity = capacity_tokens;
   h->W = (capacity_tokens + 63) / 64;
   h->tokens = 0;
-  // one allocation, so that a reset is one fill: the history, then the counters
-  h->words = (int64_t)E * h->W + ((int64_t)E * E + 1) / 2 + 3;
+  // one allocation: the history, the counter copies, the snapshot, the finalize words
+  const int64_t mat_words = ((int64_t)E * E + 1) / 2;  // one E x E uint32 matrix, in u64 words
+  h->words = (int64_t)E * h->W + (kStreamCopies + 1) * mat_words + 4;
+  h->copies_clean = true;
+  h->snap_valid = false;
+  h->hist_dirty = 0;
   hipError_t e = hipGetDevice(&h->device);
   if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&h->hist), (size_t)h->words * sizeof(u64));
   if (e == hipSuccess) {
-    h->cacc = reinterpret_cast<uint32_t*>(h->hist + (int64_t)E * h->W);
-    h->fin = h->hist + (int64_t)E * h->W + ((int64_t)E * E + 1) / 2;
+    u64* c = h->hist + (int64_t)E * h->W;
+    h->cacc = reinterpret_cast<uint32_t*>(c);
+    h->snap = reinterpret_cast<uint32_t*>(c + kStreamCopies * mat_words);
+    h->fin = c + (kStreamCopies + 1) * mat_words;
     e = hipMemset(h->hist, 0, (size_t)h->words * sizeof(u64));
   }
   if (e == hipSuccess) e = hipDeviceSynchronize();
@@ -377,6 +399,13 @@ do_status check_handle(const do_stream* h) {
   return DO_OK;
 }
 
+// Zeroes words [w0, w1) of every expert row of the history.
+hipError_t clear_history_words(do_stream* h, int64_t w0, int64_t w1, hipStream_t s) {
+  if (w1 <= w0) return hipSuccess;
+  if (w0 == 0 && w1 == h->W) return dol::launch_fill_u64(h->hist, (int64_t)h->E * h->W, s);
+  return dol::launch_fill_rows(h->hist, h->W, h->E, w0, w1 - w0, s);
+}
+
 do_status stream_append(do_stream* h, const void* const* scores, do_dtype dtype, int64_t n, int32_t count,
                         hipStream_t stream) {
   DO_TRY(check_handle(h));
@@ -391,6 +420,18 @@ do_status stream_append(do_stream* h, const void* const* scores, do_dtype dtype,
   }
   if ((h->capacity - h->tokens) / count < n)
     return fail(DO_ERR_CAPACITY, "append would exceed the history capacity");
+  // Words that this append writes.  When the micro-batches start and end on
+  // word boundaries every word is written whole by exactly one of them, with
+  // plain stores.  Otherwise words shared between micro-batches are OR-ed, so
+  // words not yet written in this epoch that may still hold bits from before
+  // the last reset are cleared first.
+  const int64_t w_fresh = (h->tokens + 63) / 64;  // first word with no bits of this epoch
+  const int64_t w_end = (h->tokens + (int64_t)count * n + 63) / 64;
+  const bool aligned_words = (h->tokens % 64) == 0 && (n % 64) == 0;
+  if (!aligned_words && w_fresh < h->hist_dirty) {
+    DO_TRY(hip_status(clear_history_words(h, w_fresh, h->hist_dirty, stream), "history clear"));
+    h->hist_dirty = w_fresh;
+  }
   dol::PathArgs a{};
   a.E = h->E;
   a.k = h->k;
@@ -398,8 +439,11 @@ do_status stream_append(do_stream* h, const void* const* scores, do_dtype dtype,
   a.bits_layer_words = (int64_t)h->E * h->W;
   a.W = h->W;
   a.or_partial = 1;
-  a.cacc = h->E <= dol::kFastMaxE ? h->cacc : nullptr;  // wider E: Gram of the whole history at finalize
+  const bool gram = h->E <= dol::kFastMaxE;  // wider E: Gram of the whole history at finalize
+  a.cacc = gram ? h->cacc : nullptr;
   a.cacc_layer_elems = (int64_t)h->E * h->E;
+  a.ncopies = kStreamCopies;
+  a.cacc_copy_elems = 2 * (((int64_t)h->E * h->E + 1) / 2);
   dol::SegTable tab{};
   for (int i = 0; i < count; ++i) {
     tab.s[i].scores = scores[i];
@@ -410,6 +454,8 @@ do_status stream_append(do_stream* h, const void* const* scores, do_dtype dtype,
   DO_TRY(hip_status(profiled(stream, [&] { return dol::launch_topk(dtype, tab, count, a, fast, stream); }),
                     "stream append"));
   h->tokens += (int64_t)count * n;
+  h->hist_dirty = std::max(h->hist_dirty, w_end);
+  if (gram) h->copies_clean = false;
   return DO_OK;
 }
 
@@ -432,16 +478,32 @@ DOLOSS_API do_status do_stream_finalize(do_stream* h, uint32_t* D, do_loss_resul
   DO_TRY(check_handle(h));
   if (D == nullptr || !aligned(D, 4)) return fail(DO_ERR_INVALID_ARG, "D is NULL or not 4-byte aligned");
   if (out == nullptr || !aligned(out, 8)) return fail(DO_ERR_INVALID_ARG, "out is NULL or not 8-byte aligned");
-  if (h->E <= dol::kFastMaxE)
-    return hip_status(dol::launch_finalize_split(h->cacc, D, out, h->E, h->fin, stream), "finalize");
+  if (h->E <= dol::kFastMaxE) {
+    const int64_t copy_elems = 2 * (((int64_t)h->E * h->E + 1) / 2);
+    DO_TRY(hip_status(dol::launch_finalize_stream(h->cacc, kStreamCopies, copy_elems, h->snap, h->snap_valid ? 1 : 0,
+                                                  D, out, h->E, h->fin, stream),
+                      "finalize"));
+    h->copies_clean = true;  // the totals now live in the snapshot
+    h->snap_valid = true;
+    return DO_OK;
+  }
+  // wider E: the Gram of the words holding this epoch's tokens
   DO_TRY(hip_status(dol::launch_fill_u32(D, (int64_t)h->E * h->E, 0u, stream), "fill"));
-  DO_TRY(hip_status(dol::launch_gram_bits(h->hist, h->W, h->E, 1, D, stream), "gram"));
+  DO_TRY(hip_status(dol::launch_gram_bits(h->hist, (h->tokens + 63) / 64, h->W, h->E, 1, D, stream), "gram"));
   return hip_status(dol::launch_finalize(D, D, out, h->E, 1, stream), "finalize");
 }
 
 DOLOSS_API do_status do_stream_reset(do_stream* h, hipStream_t stream) {
   DO_TRY(check_handle(h));
-  DO_TRY(hip_status(dol::launch_fill_u64(h->hist, h->words, stream), "reset"));  // history and counters
+  // The history is cleared lazily (see stream_append); the counter copies
+  // need a clear only if an append added to them since the last finalize.
+  if (!h->copies_clean) {
+    const int64_t mat_words = ((int64_t)h->E * h->E + 1) / 2;
+    DO_TRY(hip_status(dol::launch_fill_u64(reinterpret_cast<u64*>(h->cacc), kStreamCopies * mat_words, stream),
+                      "reset"));
+    h->copies_clean = true;
+  }
+  h->snap_valid = false;
   h->tokens = 0;
   return DO_OK;
 }

@@ -47,9 +47,10 @@ struct PathArgs {
   int64_t bits_layer_words; // words per layer of `bits`
   int64_t W;                // words per expert row of `bits`
   int32_t or_partial;       // words shared with other segments are OR-ed (history), else stored
-  int32_t pad_;
+  int32_t ncopies;          // copies of the accumulators (0 or 1: one); block b adds into copy b % ncopies
   uint32_t* cacc;           // nullable: co-occurrence accumulators [layer][E][E], upper triangle
   int64_t cacc_layer_elems;
+  int64_t cacc_copy_elems;  // distance between copies
 };
 
 // Arguments of the surrogate-loss kernel.
@@ -74,13 +75,17 @@ DevInfo device_info();
 
 hipError_t launch_fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s);
 hipError_t launch_fill_u64(u64* p, int64_t n, hipStream_t s);
+// Zeroes words [w0, w0 + nw) of `rows` rows that are ld words apart.
+hipError_t launch_fill_rows(u64* p, int64_t ld, int32_t rows, int64_t w0, int64_t nw, hipStream_t s);
 
 // Top-K signatures of `nseg` segments; with a.cacc also the co-occurrence
 // counts of each segment's tokens added into a.cacc (popcount Gram).
 hipError_t launch_topk(do_dtype dt, SegTable& tab, int nseg, const PathArgs& a, bool fast_ok, hipStream_t s);
 
-// Co-occurrence counts of existing signatures: cacc[l][i][j] += popcount(F_i & F_j), i <= j.
-hipError_t launch_gram_bits(const u64* bits, int64_t W, int32_t E, int32_t L, uint32_t* cacc, hipStream_t s);
+// Co-occurrence counts of existing signatures: cacc[l][i][j] += popcount(F_i & F_j), i <= j,
+// over the first W words of rows that are ld words apart (layers E * ld words apart).
+hipError_t launch_gram_bits(const u64* bits, int64_t W, int64_t ld, int32_t E, int32_t L, uint32_t* cacc,
+                            hipStream_t s);
 // The same Gram on fp4 MFMA tiles (E <= 256): counts added into cacc [L][E][E]
 // (upper triangle, zeroed by the caller).
 hipError_t launch_gram_mfma(const u64* bits, int64_t W, int32_t E, int32_t L, uint32_t* cacc, hipStream_t s);
@@ -128,5 +133,14 @@ hipError_t launch_rem_dispatch(const do_rem_move* replicas, const int32_t* n_rep
 hipError_t launch_finalize_split(const uint32_t* cacc, uint32_t* D, do_loss_result* out, int32_t E, u64* fin,
                                  hipStream_t s);
 hipError_t launch_loss(const uint32_t* D, int32_t E, int32_t L, do_loss_result* out, hipStream_t s);
+
+// The stream's finalize (one layer, E <= 256): the co-occurrence counts are
+// snap (if snap_valid) plus the sum of the ncopies copies (copy_elems apart);
+// writes D and out, then stores the totals in snap and zeroes the copies, so
+// that a repeated finalize gives the same result.  fin: three u64, zero before
+// and after.
+hipError_t launch_finalize_stream(uint32_t* copies, int32_t ncopies, int64_t copy_elems, uint32_t* snap,
+                                  int32_t snap_valid, uint32_t* D, do_loss_result* out, int32_t E, u64* fin,
+                                  hipStream_t s);
 
 }  // namespace dol

@@ -46,18 +46,25 @@ __global__ void k_fill_u64(u64* p, int64_t n) {
   }
 }
 
+// Zeroes words [w0, w0 + nw) of `rows` rows that are ld words apart.
+__global__ void k_fill_rows(u64* p, int64_t ld, int rows, int64_t w0, int64_t nw) {
+  const int64_t total = (int64_t)rows * nw;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x)
+    p[(i / nw) * ld + w0 + i % nw] = 0ull;
+}
+
 // grid = (word-chunk blocks, micro-tile slices, layers).  Each thread owns up
 // to kGramMtq 4x4 micro-tiles of the upper triangle and accumulates
 // popcount(F_i & F_j) over the word chunks of its block in registers.
-__global__ __launch_bounds__(kGramThreads) void k_gram_bits(const u64* __restrict__ bits, int64_t W, int E,
-                                                            uint32_t* __restrict__ cacc) {
+__global__ __launch_bounds__(kGramThreads) void k_gram_bits(const u64* __restrict__ bits, int64_t W, int64_t ld,
+                                                            int E, uint32_t* __restrict__ cacc) {
   extern __shared__ __align__(16) u64 tile[];  // [kGramSlots][E4]
   const int E4 = (E + 3) & ~3;
   const int NB = E4 / 4;
   const int NMT = NB * (NB + 1) / 2;
   const int tid = threadIdx.x;
   const int layer = blockIdx.z;
-  const u64* lb = bits + (int64_t)layer * E * W;
+  const u64* lb = bits + (int64_t)layer * E * ld;
 
   int ra[kGramMtq], rb[kGramMtq];
   uint32_t acc[kGramMtq][16];
@@ -94,7 +101,7 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bits(const u64* __restric
       for (int b = 0; b < kB; ++b) {
         const int f = f0 + b * kGramThreads, e = f / kGramSlots, s = f % kGramSlots;
         const bool in = f < total && e < E && w0 + s < W;
-        v[b] = lb[in ? (int64_t)e * W + w0 + s : 0];
+        v[b] = lb[in ? (int64_t)e * ld + w0 + s : 0];
         v[b] = in ? v[b] : 0ull;
       }
 #pragma unroll
@@ -346,6 +353,83 @@ __device__ void block_sum3(u64& s1, u64& s2h, u64& s2l) {
   }
 }
 
+// The stream's finalize (one layer, E <= 256), over ceil(E/8) blocks of 512
+// threads with wave w of block b on row 8b + w, as k_finalize_split.  The
+// co-occurrence count c_ij is snap_ij (when snap_valid) plus the sum of the
+// ncopies counter copies.  Each row's owner stores the totals of its
+// off-diagonal entries in snap and zeroes them in the copies right after
+// reading them; the diagonal, which every block reads, is moved into snap by
+// the block that takes the last ticket.  A repeated finalize therefore reads
+// the same totals (snap plus zero copies).
+__global__ __launch_bounds__(512) void k_finalize_stream(uint32_t* copies, int ncopies, int64_t copy_elems,
+                                                         uint32_t* snap, int snap_valid, uint32_t* __restrict__ d,
+                                                         do_loss_result* out, int E, u64* fin) {
+  __shared__ uint32_t diag[kFastMaxE];
+  __shared__ int last;
+  for (int i = threadIdx.x; i < E; i += blockDim.x) {
+    const int64_t o = (int64_t)i * E + i;
+    uint32_t v = snap_valid ? snap[o] : 0u;
+    for (int c = 0; c < ncopies; ++c) v += copies[c * copy_elems + o];
+    diag[i] = v;
+  }
+  __syncthreads();
+  const int w = (int)(threadIdx.x >> 6), lane = (int)(threadIdx.x & 63);
+  const int i = (int)blockIdx.x * kSplitRows + w;
+  u64 s1 = 0, s2 = 0;
+  if (i < E) {
+    const int64_t row = (int64_t)i * E;
+    if (lane == 0) d[row + i] = 0u;
+    const uint32_t di = diag[i];
+    uint32_t tot[kFastMaxE / 64];
+    // every load of the row (snapshot and copies) is issued before any store
+#pragma unroll
+    for (int q = 0; q < kFastMaxE / 64; ++q) {
+      const int j = lane + 64 * q;
+      const bool in = j > i && j < E;
+      const int64_t o = row + (in ? j : i);
+      uint32_t v = (snap_valid && in) ? snap[o] : 0u;
+      for (int c = 0; c < ncopies; ++c) v += in ? copies[c * copy_elems + o] : 0u;
+      tot[q] = v;
+    }
+#pragma unroll
+    for (int q = 0; q < kFastMaxE / 64; ++q) {
+      const int j = lane + 64 * q;
+      if (j > i && j < E) {
+        const uint32_t v = di + diag[j] - 2u * tot[q];
+        d[row + j] = v;
+        d[(int64_t)j * E + i] = v;
+        s1 += 2ull * v;
+        s2 += 2ull * (u64)v * (u64)v;
+        snap[row + j] = tot[q];
+        for (int c = 0; c < ncopies; ++c) copies[c * copy_elems + row + j] = 0u;
+      }
+    }
+  }
+  block_sum2(s1, s2);
+  if (threadIdx.x == 0) {
+    atomicAdd(&fin[0], s1);
+    atomicAdd(&fin[1], s2);
+    __threadfence();
+    last = atomicAdd(&fin[2], 1ull) == (u64)gridDim.x - 1;
+  }
+  __syncthreads();
+  if (!last) return;
+  // every block has read the diagonal: move it into the snapshot
+  __threadfence();
+  for (int j = threadIdx.x; j < E; j += blockDim.x) {
+    const int64_t o = (int64_t)j * E + j;
+    snap[o] = diag[j];
+    for (int c = 0; c < ncopies; ++c) copies[c * copy_elems + o] = 0u;
+  }
+  if (threadIdx.x == 0) {
+    const u64 S1 = atomicAdd(&fin[0], 0ull), S2 = atomicAdd(&fin[1], 0ull);
+    write_result(out, S1, 0ull, S2, E);
+    atomicExch(&fin[0], 0ull);
+    atomicExch(&fin[1], 0ull);
+    atomicExch(&fin[2], 0ull);
+  }
+}
+
 // Sums of a stored D (every off-diagonal entry), 8 rows per wave per pass.
 // Entries are arbitrary u32 values, so the sum of squares is kept in 128
 // bits per lane (one entry's square alone may reach 2^64 - 2^33 + 1).
@@ -414,7 +498,8 @@ hipError_t launch_fill_u64(u64* p, int64_t n, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_gram_bits(const u64* bits, int64_t W, int32_t E, int32_t L, uint32_t* cacc, hipStream_t s) {
+hipError_t launch_gram_bits(const u64* bits, int64_t W, int64_t ld, int32_t E, int32_t L, uint32_t* cacc,
+                            hipStream_t s) {
   const int E4 = (E + 3) & ~3;
   const int NB = E4 / 4;
   const int NMT = NB * (NB + 1) / 2;
@@ -429,7 +514,7 @@ hipError_t launch_gram_bits(const u64* bits, int64_t W, int32_t E, int32_t L, ui
   int64_t bx = ((int64_t)di.cu_count * 4 + (int64_t)slices * L - 1) / ((int64_t)slices * L);
   bx = std::max<int64_t>(1, std::min<int64_t>(bx, nchunks));
   hipLaunchKernelGGL(k_gram_bits, dim3((unsigned)bx, (unsigned)slices, (unsigned)L), dim3(kGramThreads), lds, s,
-                     bits, W, E, cacc);
+                     bits, W, ld, E, cacc);
   return hipGetLastError();
 }
 
@@ -444,6 +529,23 @@ hipError_t launch_finalize_split(const uint32_t* cacc, uint32_t* D, do_loss_resu
   if (E > kFastMaxE) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_finalize_split, dim3((unsigned)((E + kSplitRows - 1) / kSplitRows)), dim3(kSplitRows * kWave), 0,
                      s, cacc, D, out, E, fin);
+  return hipGetLastError();
+}
+
+hipError_t launch_finalize_stream(uint32_t* copies, int32_t ncopies, int64_t copy_elems, uint32_t* snap,
+                                  int32_t snap_valid, uint32_t* D, do_loss_result* out, int32_t E, u64* fin,
+                                  hipStream_t s) {
+  if (E > kFastMaxE) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_finalize_stream, dim3((unsigned)((E + kSplitRows - 1) / kSplitRows)), dim3(kSplitRows * kWave),
+                     0, s, copies, ncopies, copy_elems, snap, snap_valid, D, out, E, fin);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_rows(u64* p, int64_t ld, int32_t rows, int64_t w0, int64_t nw, hipStream_t s) {
+  if (rows <= 0 || nw <= 0) return hipSuccess;
+  const int64_t total = (int64_t)rows * nw;
+  const int64_t blocks = std::min<int64_t>((total + 255) / 256, 4096);
+  hipLaunchKernelGGL(k_fill_rows, dim3((unsigned)blocks), dim3(256), 0, s, p, ld, rows, w0, nw);
   return hipGetLastError();
 }
 

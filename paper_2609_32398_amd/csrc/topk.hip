@@ -132,49 +132,90 @@ __device__ __forceinline__ void insert8(int (&top)[8], int x, int& rej) {
   top[0] = max(top[0], x);
 }
 
-// (x & mask) | (y & ~mask) in one instruction.  Written out because the
-// compiler otherwise splits it into AND + OR: gfx9 VOP3 encodings take no
-// literal, so the mask sits in a VGPR and the expert index in an SGPR.
-__device__ __forceinline__ uint32_t bfi(uint32_t vmask, uint32_t x, uint32_t sidx) {
+// The index part of the composite keys: byte b of word w is 255 - (4w + b),
+// the complemented expert index of expert 4w + b.  A chunk's index bytes are
+// read with one scalar load and each key takes its byte with one v_perm_b32,
+// so building a key costs no scalar instruction for its index constant.
+struct IdxTab {
+  uint32_t w[kFastMaxE / 4];
+};
+constexpr IdxTab make_idx_tab() {
+  IdxTab t{};
+  for (int i = 0; i < kFastMaxE / 4; ++i) {
+    uint32_t v = 0;
+    for (int b = 0; b < 4; ++b) v |= (uint32_t)(255 - (4 * i + b)) << (8 * b);
+    t.w[i] = v;
+  }
+  return t;
+}
+__constant__ IdxTab kIdxTab = make_idx_tab();
+
+// v_perm_b32: byte i of the result is byte sel.byte[i] of {x (bytes 4-7),
+// sidx (bytes 0-3)}, 12 selects 0x00.  sidx is a scalar (the index bytes),
+// sel a loop-invariant VGPR.
+__device__ __forceinline__ uint32_t perm(uint32_t x, uint32_t sidx, uint32_t sel) {
   uint32_t r;
-  asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(r) : "v"(vmask), "v"(x), "s"(sidx));
+  asm("v_perm_b32 %0, %1, %2, %3" : "=v"(r) : "v"(x), "s"(sidx), "v"(sel));
   return r;
 }
 
-// Composite keys.  e: expert index (< 256).  vm24 = 0xFFFFFF00, vm16 = 0xFFFF0000 (VGPRs).
+// Byte selectors of the composite keys (VGPRs set once per kernel).
+//   f32[j]: [index byte j, x.b1, x.b2, x.b3]                 -> value bits 8..31, index
+//   lo[j]:  [index byte j, 0, x.b0, x.b1] (bf16 in the low half)
+//   hi[j]:  [index byte j, 0, x.b2, x.b3] (bf16 in the high half)
+struct KeySel {
+  uint32_t f32[4];
+  uint32_t lo[2];  // index bytes 0 and 2
+  uint32_t hi[2];  // index bytes 1 and 3
+};
+
+// Composite keys.  idx: scalar holding the index bytes of 4 consecutive experts.
 template <bool GEN>
-__device__ __forceinline__ int key_f32(uint32_t u, int e, uint32_t vm24) {
+__device__ __forceinline__ int key_f32(uint32_t u, uint32_t idx, uint32_t sel) {
   if (GEN) u ^= (uint32_t)((int32_t)u >> 31) & 0x7FFFFF00u;
-  return (int)bfi(vm24, u, (uint32_t)(255 - e));
+  return (int)perm(u, idx, sel);
 }
 
-// Two bf16 scores packed in x (element e0 in the low half, e0 + 1 in the high half).
+// Two bf16 scores packed in x (the even expert in the low half), their index
+// bytes in bytes 2h and 2h + 1 of idx.
 template <bool GEN>
-__device__ __forceinline__ void key_bf16x2(uint32_t x, int e0, uint32_t vm16, int& lo, int& hi) {
+__device__ __forceinline__ void key_bf16x2(uint32_t x, uint32_t idx, int h, const KeySel& ks, int& lo, int& hi) {
   if (GEN) {
     const v2s s = __builtin_bit_cast(v2s, x) >> (short)15;
     x ^= __builtin_bit_cast(uint32_t, s) & 0x7FFF7FFFu;
   }
-  lo = (int)((x << 16) | (uint32_t)(255 - e0));
-  hi = (int)bfi(vm16, x, (uint32_t)(254 - e0));
+  lo = (int)perm(x, idx, ks.lo[h]);
+  hi = (int)perm(x, idx, ks.hi[h]);
 }
 
 // Rank one staged 128-byte chunk (vectors cv0..cv0+7 of the lane's row) into top/rej.
 template <typename T, bool GEN>
-__device__ __forceinline__ void rank_chunk(const unsigned char* sbuf, int lane, int cv0, uint32_t vmask,
+__device__ __forceinline__ void rank_chunk(const unsigned char* sbuf, int lane, int cv0, const KeySel& ks,
                                            int (&top)[8], int& rej) {
   const unsigned char* row = sbuf + lane * 128;
   const int sw = row_swizzle(lane);
   auto piece = [&](int q) { return *reinterpret_cast<const v4u*>(row + ((q ^ sw) << 4)); };
+  // index bytes of the chunk's experts (one scalar load: the chunk index is uniform)
+  constexpr int kWords = Traits<T>::kVec * 8 / 4;
+  const uint32_t* iw = kIdxTab.w + cv0 * (Traits<T>::kVec / 4);
+  uint32_t idx[kWords];
+#pragma unroll
+  for (int i = 0; i < kWords; ++i) idx[i] = __builtin_amdgcn_readfirstlane(iw[i]);
   if (Traits<T>::kVec == 4) {
+    // the next piece's read is issued before the current piece is ranked, and
+    // a piece's four keys are built before any is inserted
+    v4u x = piece(0);
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
-      const v4u x = piece(q);
-      const int e0 = (cv0 + q) * 4;
-      insert8<!Traits<T>::kExact>(top, key_f32<GEN>(x.x, e0 + 0, vmask), rej);
-      insert8<!Traits<T>::kExact>(top, key_f32<GEN>(x.y, e0 + 1, vmask), rej);
-      insert8<!Traits<T>::kExact>(top, key_f32<GEN>(x.z, e0 + 2, vmask), rej);
-      insert8<!Traits<T>::kExact>(top, key_f32<GEN>(x.w, e0 + 3, vmask), rej);
+      const v4u xn = piece(q + 1 < 8 ? q + 1 : q);
+      int g[4];
+      g[0] = key_f32<GEN>(x.x, idx[q], ks.f32[0]);
+      g[1] = key_f32<GEN>(x.y, idx[q], ks.f32[1]);
+      g[2] = key_f32<GEN>(x.z, idx[q], ks.f32[2]);
+      g[3] = key_f32<GEN>(x.w, idx[q], ks.f32[3]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) insert8<!Traits<T>::kExact>(top, g[i], rej);
+      x = xn;
     }
   } else {
     // all eight reads issued up front: their latency overlaps the ranking of
@@ -187,11 +228,10 @@ __device__ __forceinline__ void rank_chunk(const unsigned char* sbuf, int lane, 
     for (int v = 0; v < 8; ++v) {
       int g[8];
       const v4u x = xs[v];
-      const int e0 = (cv0 + v) * 8;
-      key_bf16x2<GEN>(x.x, e0 + 0, vmask, g[0], g[1]);
-      key_bf16x2<GEN>(x.y, e0 + 2, vmask, g[2], g[3]);
-      key_bf16x2<GEN>(x.z, e0 + 4, vmask, g[4], g[5]);
-      key_bf16x2<GEN>(x.w, e0 + 6, vmask, g[6], g[7]);
+      key_bf16x2<GEN>(x.x, idx[2 * v], 0, ks, g[0], g[1]);
+      key_bf16x2<GEN>(x.y, idx[2 * v], 1, ks, g[2], g[3]);
+      key_bf16x2<GEN>(x.z, idx[2 * v + 1], 0, ks, g[4], g[5]);
+      key_bf16x2<GEN>(x.w, idx[2 * v + 1], 1, ks, g[6], g[7]);
 #pragma unroll
       for (int i = 0; i < 8; ++i) insert8<false>(top, g[i], rej);
     }
@@ -546,14 +586,19 @@ __device__ __forceinline__ void mfma_flush(const typename Mfma<TS>::Acc (&acc)[k
 
 #define DOL_WAVE_FENCE() asm volatile("" ::: "memory")
 
-// One segment as the kernel sees it (all values wave-uniform).
+// One segment as the kernel sees it (all values wave-uniform).  Counts fit
+// 32 bits: a segment holds fewer than 2^32 tokens and its bit positions stay
+// below 2^32, so word indices are below 2^26 and unit indices below 2^29.
+// Row r of local word wl holds token wl*64 + r - sh; base points at the
+// (virtual) token -sh, so the row pointer of a word is base + wl*64*rowB.
 struct Seg {
-  const unsigned char* base;  // scores of its token 0
-  int64_t n;                  // tokens
-  int64_t off;                // bit position of its token 0 in the output rows
-  int64_t w_first;            // first signature word it touches
-  int64_t words;              // signature words it touches
-  int64_t u_begin;            // its first global unit
+  const unsigned char* base;  // scores of token -sh
+  uint32_t n;                 // tokens
+  uint32_t sh;                // bit position of token 0 within its first word
+  uint32_t w_first;           // first signature word it touches
+  uint32_t words;             // signature words it touches
+  uint32_t full_lo, full_hi;  // local words [full_lo, full_hi) hold 64 of its tokens
+  uint32_t u_begin;           // its first global unit
   int layer;
 };
 
@@ -562,23 +607,32 @@ struct Seg {
 // the compiler copy the whole table to private memory first.
 typedef const __attribute__((address_space(4))) SegTable* SegTablePtr;
 
-__device__ __forceinline__ Seg load_seg(SegTablePtr tab, int i) {
+__device__ __forceinline__ Seg load_seg(SegTablePtr tab, int i, int rowB) {
   Seg v;
-  v.base = reinterpret_cast<const unsigned char*>(tab->s[i].scores);
-  v.n = tab->s[i].n;
-  v.off = tab->s[i].tok_off;
-  v.w_first = v.off >> 6;
-  v.words = v.n > 0 ? ((v.off + v.n - 1) >> 6) - v.w_first + 1 : 0;
-  v.u_begin = tab->tile_start[i];
+  const uint64_t off = (uint64_t)tab->s[i].tok_off;
+  const uint64_t n = (uint64_t)tab->s[i].n;
+  v.n = (uint32_t)n;
+  v.sh = (uint32_t)(off & 63);
+  v.base = reinterpret_cast<const unsigned char*>(tab->s[i].scores) - (uint64_t)v.sh * (uint64_t)rowB;
+  v.w_first = (uint32_t)(off >> 6);
+  v.words = n > 0 ? (uint32_t)(((off & 63) + n + 63) >> 6) : 0u;
+  v.full_lo = v.sh != 0 ? 1u : 0u;
+  v.full_hi = (uint32_t)(((off & 63) + n) >> 6);
+  v.u_begin = (uint32_t)tab->tile_start[i];
   v.layer = tab->s[i].layer;
   return v;
 }
 
 // Segment holding global unit u (segments with no units are skipped).
-__device__ __forceinline__ int seg_of(SegTablePtr tab, int64_t u, int from) {
+__device__ __forceinline__ int seg_of(SegTablePtr tab, uint32_t u, int from) {
   int i = from;
-  while (i + 1 < tab->nseg && u >= tab->tile_start[i + 1]) ++i;
+  while (i + 1 < tab->nseg && u >= (uint32_t)tab->tile_start[i + 1]) ++i;
   return i;
+}
+
+// Row pointer of local word wl of segment sg.
+__device__ __forceinline__ const unsigned char* word_rows(const Seg& sg, uint32_t wl, int rowB) {
+  return sg.base + (uint64_t)(wl << 6) * (uint64_t)rowB;
 }
 
 typedef unsigned long long v2u64 __attribute__((ext_vector_type(2)));
@@ -600,7 +654,7 @@ typedef unsigned long long v2u64 __attribute__((ext_vector_type(2)));
 // schedule group.
 // ---------------------------------------------------------------------------
 template <typename T, int EP, int GM>
-__global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, const PathArgs a, int flags, int64_t gu) {
+__global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, const PathArgs a, int flags, uint32_t gu) {
   (void)tab_arg;  // read through `tab` below (it is the first kernel argument)
   const SegTablePtr tab = (SegTablePtr)__builtin_amdgcn_kernarg_segment_ptr();
   constexpr int EPW = EP < 32 ? 32 : EP;  // signature words per slot of the bit tile
@@ -628,22 +682,26 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
   //      blocks work on adjacent groups of its partition, so their signature
   //      stores land side by side while each block stays in few layers (few
   //      Gram flushes, and those of different XCDs go to different layers)
-  const int64_t U = tab->tile_start[tab->nseg];
-  const int G = gridDim.x;
-  const int b = blockIdx.x;
+  // All unit counts are below 2^29 (64 segments of fewer than 2^32 tokens).
+  const uint32_t U = (uint32_t)tab->tile_start[tab->nseg];
+  const uint32_t G = gridDim.x;
+  const uint32_t b = blockIdx.x;
   const bool xcd = (G & 7) == 0 && (flags & 2) != 0;
-  const int64_t lo = xcd ? (int64_t)(b & 7) * U / 8 : 0;
-  const int64_t hi = xcd ? (int64_t)((b & 7) + 1) * U / 8 : U;
-  const int Gs = xcd ? G >> 3 : G;
-  const int pos = xcd ? b >> 3 : b;
-  const int64_t ug = lo + (int64_t)pos * gu;
+  const uint32_t lo = xcd ? (uint32_t)(((uint64_t)(b & 7) * U) >> 3) : 0u;
+  const uint32_t hi = xcd ? (uint32_t)(((uint64_t)((b & 7) + 1) * U) >> 3) : U;
+  const uint32_t Gs = xcd ? G >> 3 : G;
+  const uint32_t pos = xcd ? b >> 3 : b;
+  const uint32_t ug = lo + pos * gu;
   if (ug >= hi) return;
-  // unit after u in this block's schedule (U when there is none)
-  auto next_unit = [&](int64_t u_) -> int64_t {
-    const int64_t v = u_ + 1;
-    if ((v - lo) % gu != 0) return v < hi ? v : U;
-    const int64_t w = v + (int64_t)(Gs - 1) * gu;
-    return w < hi ? w : U;
+  // The unit after u in this block's schedule (U when there is none), from
+  // the bounds of the current group: called once per unit, in order.
+  uint32_t g_start = ug, g_end = min(ug + gu, hi);
+  auto next_unit = [&](uint32_t u_) -> uint32_t {
+    if (u_ + 1 < g_end) return u_ + 1;
+    g_start += Gs * gu;
+    if (g_start >= hi) return U;
+    g_end = min(g_start + gu, hi);
+    return g_start;
   };
 
   PopcGram<EPW, kFusedThreads, GM == kGramPopc> pg;
@@ -665,25 +723,24 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
   const uint32_t off_even = (uint32_t)((lane >> 3) * rowB + q_even * 16);        // bytes from the chunk's row 0
   const uint32_t off_odd = (uint32_t)((lane >> 3) * rowB + (q_even ^ 1) * 16);  // odd j: piece q_even ^ 1
 
-  // Direct-to-LDS load of full 128-byte chunk c_ of the 64 rows starting at
-  // token t0_ of segment sg (asynchronous; the consumer waits with DOL_WAIT_VMEM).
-  // Rows r = 8 j + lane/8 of the 64 starting at token t0_ that lie inside the
-  // segment: [r_lo, r_hi) (wave-uniform, 32-bit compares per lane).
+  // Rows [r_lo, r_hi) of local word wl of segment sg hold its tokens
+  // (wave-uniform; 64-bit only where sh + n may reach 2^32).
   const int row_in_j0 = lane >> 3;
-  auto row_bounds = [&](const Seg& sg, int64_t t0_, int& r_lo, int& r_hi) {
-    r_lo = (int)min((int64_t)64, max((int64_t)0, -t0_));
-    r_hi = (int)max((int64_t)0, min((int64_t)64, sg.n - t0_));
+  auto row_bounds = [&](const Seg& sg, uint32_t wl, int& r_lo, int& r_hi) {
+    r_lo = wl == 0 ? (int)sg.sh : 0;
+    const int64_t rem = (int64_t)sg.sh + (int64_t)sg.n - ((int64_t)wl << 6);
+    r_hi = (int)max((int64_t)0, min((int64_t)64, rem));
   };
-  // Direct-to-LDS load of full 128-byte chunk c_ of the 64 rows starting at
-  // token t0_ of segment sg (asynchronous; the consumer waits with
-  // DOL_WAIT_VMEM).  When every row lies inside the segment the loads go
-  // through a buffer resource based at the chunk's row 0: the row offsets are
-  // scalar and the lane offset is one 32-bit register, so issuing a load
-  // costs no vector instruction.
-  auto dma = [&](const Seg& sg, int64_t t0_, int c_, unsigned char* sbuf) {
+  // Direct-to-LDS load of full 128-byte chunk c_ of the 64 rows of local word
+  // wl of segment sg (asynchronous; the consumer waits with DOL_WAIT_VMEM).
+  // When every row lies inside the segment the loads go through a buffer
+  // resource based at the chunk's row 0: the row offsets are scalar and the
+  // lane offset is one 32-bit register, so issuing a load costs no vector
+  // instruction.
+  auto dma = [&](const Seg& sg, uint32_t wl, int c_, unsigned char* sbuf) {
     if (c_ * 8 + 8 > rowv) return;
-    const unsigned char* cbase = sg.base + t0_ * rowB + c_ * 128;  // row 0 of the chunk (uniform)
-    if (t0_ >= 0 && t0_ + 64 <= sg.n) {  // every row inside the segment
+    const unsigned char* cbase = word_rows(sg, wl, rowB) + c_ * 128;  // row 0 of the chunk (uniform)
+    if (wl >= sg.full_lo && wl < sg.full_hi) {  // every row inside the segment
       const __amdgpu_buffer_rsrc_t rs =
           __builtin_amdgcn_make_buffer_rsrc(const_cast<unsigned char*>(cbase), (short)0, 0x7FFFFFFF, kBufWord3);
 #pragma unroll
@@ -693,7 +750,7 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
                                                  kStreamPolicy);
     } else {
       int r_lo, r_hi;
-      row_bounds(sg, t0_, r_lo, r_hi);
+      row_bounds(sg, wl, r_lo, r_hi);
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         const int r = 8 * j + row_in_j0;
@@ -705,11 +762,11 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
   };
   // Synchronous fill of a partial chunk (the row ends inside it): missing
   // vectors read as all-ones (a NaN), ranked last and never selected on the fast path.
-  auto fill_partial = [&](const Seg& sg, int64_t t0_, int c_, unsigned char* sbuf) {
+  auto fill_partial = [&](const Seg& sg, uint32_t wl, int c_, unsigned char* sbuf) {
     const int cvn = rowv - c_ * 8;
-    const unsigned char* cbase = sg.base + t0_ * rowB + c_ * 128;
+    const unsigned char* cbase = word_rows(sg, wl, rowB) + c_ * 128;
     int r_lo, r_hi;
-    row_bounds(sg, t0_, r_lo, r_hi);
+    row_bounds(sg, wl, r_lo, r_hi);
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int r = 8 * j + row_in_j0;
@@ -764,7 +821,7 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
   // The unit whose bit tile is complete and whose stores and Gram are pending.
   struct Pending {
     u64* lb;          // bits of its layer (null: no signature output)
-    int64_t w0;       // its first signature word
+    uint32_t w0;      // its first signature word
     int cnt;          // words in it
     int layer;
     int shared_lo;    // slot 0 holds a word shared with the previous segment (OR it in)
@@ -775,7 +832,7 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
   typedef StoreBatch<EPW> SB;
   v2u64 sreg[SB::kUnits][SB::kItems];  // batched signature stores (see batch_flush)
   u64* sb_lb = nullptr;
-  int64_t sb_w0 = 0;
+  uint32_t sb_w0 = 0;
   int sb_n = 0;
   // This wave's share of the pending unit's signature stores: experts
   // [wave*E/8, (wave+1)*E/8), 64 bytes (8 words) per expert as four 16-byte
@@ -866,7 +923,8 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
   const bool pair64 = (E & 1) == 0 && (reinterpret_cast<uintptr_t>(a.cacc) & 7) == 0;
   auto flush = [&](int layer) {
     if (GM == kGramNone) return;
-    uint32_t* cl = a.cacc + (int64_t)layer * a.cacc_layer_elems;
+    uint32_t* cl = a.cacc + (int64_t)layer * a.cacc_layer_elems +
+                   (a.ncopies > 1 ? (int64_t)(blockIdx.x % (uint32_t)a.ncopies) * a.cacc_copy_elems : 0);
     if (GM == kGramMfma) {
       mfma_flush<GS::TS>(acc, wt, cl, E, lane, (int)(blockIdx.x % kGP), pair64);
       zero_acc();
@@ -884,31 +942,43 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
   // in a short launch, so bf16 starts with them.
   bool gen = Traits<T>::kExact;
   int cb = 0;  // stage buffer holding the current chunk
-  const uint32_t vmask = Traits<T>::kExact ? 0xFFFF0000u : 0xFFFFFF00u;  // value bits of a key (VGPR operand of bfi)
+  // key byte selectors, opaque to the compiler so that they stay in VGPRs
+  // instead of being rematerialised for every key
+  KeySel ks;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) ks.f32[j] = 0x07060500u | (uint32_t)j;
+  ks.lo[0] = 0x05040C00u;
+  ks.lo[1] = 0x05040C02u;
+  ks.hi[0] = 0x07060C01u;
+  ks.hi[1] = 0x07060C03u;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) asm volatile("" : "+v"(ks.f32[j]));
+#pragma unroll
+  for (int j = 0; j < 2; ++j) asm volatile("" : "+v"(ks.lo[j]), "+v"(ks.hi[j]));
 
   int seg = seg_of(tab, ug, 0);
-  Seg sv = load_seg(tab, seg);
-  int64_t tl0 = 8 * (ug - sv.u_begin);                 // local word of slot 0 of the current unit
-  int64_t t0w = (sv.w_first + tl0 + wave) * 64 - sv.off;  // token of lane 0 of this wave's word
-  if (fast && tl0 + wave < sv.words) dma(sv, t0w, 0, st);
+  Seg sv = load_seg(tab, seg, rowB);
+  uint32_t tl0 = 8 * (ug - sv.u_begin);  // local word of slot 0 of the current unit
+  if (fast && tl0 + wave < sv.words) dma(sv, tl0 + wave, 0, st);
 
   int buf = 0;
-  for (int64_t u = ug; u < U; buf ^= 1) {
-    const int cnt = (int)min((int64_t)kFusedWaves, sv.words - tl0);  // words in this unit
+  for (uint32_t u = ug; u < U; buf ^= 1) {
+    const uint32_t wl = tl0 + wave;                      // this wave's local word
+    const int cnt = (int)min((uint32_t)kFusedWaves, sv.words - tl0);  // words in this unit
     // next unit and its segment (wave-uniform)
-    const int64_t un = next_unit(u);
+    const uint32_t un = next_unit(u);
     int seg_n = seg;
     Seg svn = sv;
-    int64_t tl0n = tl0 + 8;
+    uint32_t tl0n = tl0 + 8;
     if (un < U) {
-      if (un >= tab->tile_start[seg + 1]) {
+      if (un >= (uint32_t)tab->tile_start[seg + 1]) {
         seg_n = seg_of(tab, un, seg);
-        svn = load_seg(tab, seg_n);
+        svn = load_seg(tab, seg_n, rowB);
       }
       tl0n = 8 * (un - svn.u_begin);
     }
-    const bool next_mine = un < U && tl0n + wave < svn.words;
-    const int64_t t0n = (svn.w_first + tl0n + wave) * 64 - svn.off;
+    const uint32_t wln = tl0n + wave;
+    const bool next_mine = un < U && wln < svn.words;
 
     u64* bt = bt_all + buf * kFusedWaves * EPW;
     const u64* pbt = bt_all + (buf ^ 1) * kFusedWaves * EPW;  // the pending unit's tile
@@ -922,11 +992,13 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
     if (fast && wave >= cnt && next_mine) {
       // idle in this unit (segment end) but busy in the next one: start that
       // word's first chunk now, into the buffer the next unit reads first
-      dma(svn, t0n, 0, st + cb * kChunkBytes);
+      dma(svn, wln, 0, st + cb * kChunkBytes);
     }
     if (wave < cnt) {
-      const int64_t t = t0w + lane;
-      const bool valid = (t >= 0) && (t < sv.n);
+      // the lane's row holds a token of the segment (every row of an interior word does)
+      const uint32_t row = (wl << 6) + (uint32_t)lane;
+      const bool valid = (wl >= sv.full_lo && wl < sv.full_hi) ||
+                         (row >= sv.sh && (uint64_t)row < (uint64_t)sv.sh + (uint64_t)sv.n);
       bool need_slow = valid;
       if (fast) {
         int top[8];
@@ -938,22 +1010,22 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
           if (c * 8 + 8 <= rowv) {
             DOL_WAIT_VMEM();  // this chunk's direct-to-LDS loads (and earlier stores) have completed
           } else {
-            fill_partial(sv, t0w, c, cur);
+            fill_partial(sv, wl, c, cur);
           }
           DOL_WAVE_FENCE();
           unsigned char* other = st + (cb ^ 1) * kChunkBytes;
           if (c + 1 < nch)
-            dma(sv, t0w, c + 1, other);
+            dma(sv, wl, c + 1, other);
           else if (next_mine)
-            dma(svn, t0n, 0, other);
+            dma(svn, wln, 0, other);
           if (!stored) {
             store_share(pbt);
             stored = true;
           }
           if (gen)
-            rank_chunk<T, true>(cur, lane, c * 8, vmask, top, rej);
+            rank_chunk<T, true>(cur, lane, c * 8, ks, top, rej);
           else
-            rank_chunk<T, false>(cur, lane, c * 8, vmask, top, rej);
+            rank_chunk<T, false>(cur, lane, c * 8, ks, top, rej);
           if (gram_done < kFusedWaves) {
             const int s_end = (((c + 1) * kFusedWaves) / nch) & ~(kGramStep - 1);
             gram_slots(pbt, gram_done, s_end);
@@ -962,11 +1034,18 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
           DOL_WAVE_FENCE();
           cb ^= 1;
         }
-        int sk = INT_MIN, sk1 = rej;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          sk = (i == k - 1) ? top[i] : sk;
-          sk1 = (i == k) ? top[i] : sk1;
+        // the k-th and (k+1)-th keys: a wave-uniform branch on k, so that no
+        // per-position predicate on k stays live (in registers) across the loop
+        int sk, sk1;
+        switch (k) {
+          case 1: sk = top[0]; sk1 = top[1]; break;
+          case 2: sk = top[1]; sk1 = top[2]; break;
+          case 3: sk = top[2]; sk1 = top[3]; break;
+          case 4: sk = top[3]; sk1 = top[4]; break;
+          case 5: sk = top[4]; sk1 = top[5]; break;
+          case 6: sk = top[5]; sk1 = top[6]; break;
+          case 7: sk = top[6]; sk1 = top[7]; break;
+          default: sk = top[7]; sk1 = rej; break;
         }
         bool ok = top[0] < kCompPosInf;
         bool nonpos = false;
@@ -983,10 +1062,11 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
         need_slow = valid && !ok;
         int need = 0;
         if (valid && ok) {
+          // keys are unique, so the k selected entries are those >= sk
           const u64 bit = 1ull << lane;
 #pragma unroll
           for (int i = 0; i < 8; ++i) {
-            if (i < k) {
+            if (top[i] >= sk) {
               if (!tie || (top[i] >> 8) > (sk >> 8))
                 atomicOr(&mybt[(255 - (top[i] & 255)) ^ bt_swz(wave)], bit);
               else
@@ -996,19 +1076,19 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
         }
         if (!Traits<T>::kExact) {
           const u64 tm = __ballot(tie);
-          if (tm != 0ull) resolve_ties(tm, sk, need, gen, mybt, sv.base + t0w * rowB);
+          if (tm != 0ull) resolve_ties(tm, sk, need, gen, mybt, word_rows(sv, wl, rowB));
         }
         if (__ballot(nonpos) != 0ull) gen = true;
       }
       if (__ballot(need_slow) != 0ull) {
         if (need_slow) {
-          const T* row = reinterpret_cast<const T*>(sv.base) + t * (int64_t)E;
+          const T* rp = reinterpret_cast<const T*>(word_rows(sv, wl, rowB) + (uint32_t)lane * (uint32_t)rowB);
           if (k <= 8)
-            exact_topk_list_lane<T, 8>(row, E, k, mybt, bt_swz(wave), 1ull << lane);
+            exact_topk_list_lane<T, 8>(rp, E, k, mybt, bt_swz(wave), 1ull << lane);
           else if (k <= 16)
-            exact_topk_list_lane<T, 16>(row, E, k, mybt, bt_swz(wave), 1ull << lane);
+            exact_topk_list_lane<T, 16>(rp, E, k, mybt, bt_swz(wave), 1ull << lane);
           else
-            exact_topk_passes_lane<T>(row, E, k, mybt, bt_swz(wave), 1ull << lane);
+            exact_topk_passes_lane<T>(rp, E, k, mybt, bt_swz(wave), 1ull << lane);
         }
       }
     }
@@ -1026,14 +1106,13 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
     pend.w0 = sv.w_first + tl0;
     pend.cnt = cnt;
     pend.layer = sv.layer;
-    pend.shared_lo = a.or_partial && tl0 == 0 && (sv.off & 63) != 0;
-    pend.shared_hi = (a.or_partial && tl0 + cnt == sv.words && ((sv.off + sv.n) & 63) != 0) ? cnt - 1 : -1;
+    pend.shared_lo = a.or_partial && tl0 == 0 && sv.sh != 0;
+    pend.shared_hi = (a.or_partial && tl0 + cnt == sv.words && ((sv.sh + sv.n) & 63) != 0) ? cnt - 1 : -1;
     have_pend = true;
     u = un;
     seg = seg_n;
     sv = svn;
     tl0 = tl0n;
-    t0w = t0n;
   }
   // the last unit
   store_share(bt_all + (buf ^ 1) * kFusedWaves * EPW);
@@ -1075,7 +1154,7 @@ hipError_t launch_one(const SegTable& tab, const PathArgs& a, bool fast, Sched s
   const int64_t gs = sc.xcd ? std::max<int64_t>(blocks / 8, 1) : blocks;
   if (gu <= 0 || gu * gs > per_part) gu = (per_part + gs - 1) / gs;  // contiguous ranges
   const int flags = (fast ? 1 : 0) | (sc.xcd ? 2 : 0);
-  hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kFusedThreads), lds, s, tab, a, flags, gu);
+  hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kFusedThreads), lds, s, tab, a, flags, (uint32_t)gu);
   return hipGetLastError();
 }
 

@@ -309,19 +309,67 @@ def test_stream_unaligned_appends_equal_one_batch(dl, orc, syn):
     hist = s.history()
     torch.cuda.synchronize()
     np.testing.assert_array_equal(bits_np(hist)[:, : words.shape[1]], words)
-    assert not bits_np(hist)[:, words.shape[1]:].any()
-    # finalize twice gives the same answer; reset clears everything
+    assert not bits_np(hist)[:, words.shape[1]:].any()  # never-used words are zero before any reset
+    # finalize twice gives the same answer; after a reset nothing is counted
     D2, out2 = s.finalize()
     torch.cuda.synchronize()
-    assert torch.equal(D, D2)
+    assert torch.equal(D, D2) and torch.equal(out, out2)
     s.reset()
     D3, out3 = s.finalize()
     torch.cuda.synchronize()
     assert s.tokens == 0 and int(D3.abs().sum()) == 0
-    # the reset fill covers the whole history (12,099 words here: the four-store
-    # passes, the single-store tail and the odd last word)
-    assert not bits_np(s.history()).any(), "history not cleared by the reset"
+    assert dl.loss_records(out3)[0]["sum"] == 0
+    # the old bits stay in the history after the reset; unaligned appends that
+    # follow must not OR into them: a new epoch with another split of fewer
+    # tokens gives the oracle's words over the tokens it holds
+    sizes2 = [70, 1, 129, 64, 500]
+    parts2 = [syn.normal(700 + i, n, E, 1) for i, n in enumerate(sizes2)]
+    for p in parts2:
+        s.append(to_dev(p))
+    D4, out4 = s.finalize()
+    hist4 = s.history()
+    torch.cuda.synchronize()
+    F2, words2, ref_D2, ref_L2 = orc.run_stream(parts2, k)
+    np.testing.assert_array_equal(D_np(D4), ref_D2)
+    loss_close(dl.loss_records(out4)[0], ref_L2)
+    np.testing.assert_array_equal(bits_np(hist4)[:, : words2.shape[1]], words2)
     s.close()
+
+
+@pytest.mark.parametrize("E,k,dtype", [(128, 8, 1), (256, 8, 0), (40, 5, 1)])
+def test_stream_finalize_between_appends_and_resets(dl, orc, syn, E, k, dtype):
+    """The handle's running totals: finalize after each append (the counts of
+    all tokens so far), appends after a finalize, a reset right after appends
+    (counters not yet finalized) and a reset right after a finalize."""
+    print(f"[case] stream epochs E={E} k={k} dtype={dtype}", flush=True)
+    sizes = [4096, 128, 960, 64 * 9]
+    parts = [syn.normal(1300 + 17 * i + E, n, E, dtype) for i, n in enumerate(sizes)]
+    dev = [to_dev(p) for p in parts]
+    s = dl.DoStream(E, k, sum(sizes))
+    try:
+        for epoch in range(2):
+            for upto in range(1, len(parts) + 1):
+                s.append(dev[upto - 1])
+                D, out = s.finalize()
+                torch.cuda.synchronize()
+                _, words, ref_D, ref_L = orc.run_stream(parts[:upto], k)
+                np.testing.assert_array_equal(D_np(D), ref_D, err_msg=f"epoch {epoch}, {upto} appends")
+                loss_close(dl.loss_records(out)[0], ref_L)
+                np.testing.assert_array_equal(bits_np(s.history())[:, : words.shape[1]], words)
+            s.reset()  # right after a finalize
+        # appends, then a reset before any finalize, then one aligned append
+        s.append_many(dev[:1])
+        s.append(dev[1])
+        s.reset()
+        s.append(dev[3])
+        D, out = s.finalize()
+        torch.cuda.synchronize()
+        _, words, ref_D, ref_L = orc.run_stream(parts[3:4], k)
+        np.testing.assert_array_equal(D_np(D), ref_D)
+        loss_close(dl.loss_records(out)[0], ref_L)
+        np.testing.assert_array_equal(bits_np(s.history())[:, : words.shape[1]], words)
+    finally:
+        s.close()
 
 
 def test_stream_append_many_and_capacity(dl, orc, syn):
