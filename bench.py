@@ -49,6 +49,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="oracle time to accumulate for cpu_baseline (whole layers, at least one)")
     ap.add_argument("--layers", type=int, default=None, help="override the layer count (testing only)")
+    ap.add_argument("--gram", choices=["mfma", "popc"], default="mfma",
+                    help="co-occurrence Gram inside k_topk for E <= 256: fp4 MFMA (default) or VALU popcount")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 4 GiB device copy (calibrates the HBM byte counters)")
     return ap.parse_args()
@@ -166,9 +168,11 @@ def cpu_baseline(cfg: int, seconds: float):
                 build="gcc " + " ".join(oracle.CFLAGS))
 
 
-def roofline(alg_bytes: float, kern_ms: float, workload: str, kernel: str, bytes_per_token: int) -> dict:
+def roofline(alg_bytes: float, kern_ms: float, workload: str, kernel: str, bytes_per_token: int,
+             gram: str = "mfma") -> dict:
     achieved = alg_bytes / (kern_ms / 1e3) / 1e9
-    traffic, source = recorded_traffic(workload)
+    # recorded counters cover the default (MFMA Gram) kernel only
+    traffic, source = recorded_traffic(workload) if gram == "mfma" else (None, None)
     return dict(bound="hbm", achieved=achieved, peak=HBM_PEAK_GBS, unit="GB/s", frac=achieved / HBM_PEAK_GBS,
                 traffic=traffic, traffic_source=source, kernel=kernel, kernel_ms=kern_ms,
                 algorithmic_bytes=alg_bytes, bytes_per_token=bytes_per_token)
@@ -307,9 +311,11 @@ def bench_layers(args, cfg):
         dtype="i32",
         data="synthetic",
         config=dict(workload=w["name"], layers=L, tokens_per_layer=N, experts=E, k=k,
-                    score_dtype="f32" if w["dtype"] == 0 else "bf16", signatures_written=True),
-        roofline=roofline(alg_bytes, kern_ms, w["name"], "k_topk (fused top-k, signatures, fp4 MFMA Gram)",
-                          bytes_per_token),
+                    score_dtype="f32" if w["dtype"] == 0 else "bf16", signatures_written=True,
+                    gram=args.gram),
+        roofline=roofline(alg_bytes, kern_ms, w["name"], "k_topk (fused top-k, signatures, "
+                          + ("fp4 MFMA Gram)" if args.gram == "mfma" else "popcount Gram)"),
+                          bytes_per_token, args.gram),
         step_gbs=alg_bytes / (ms_per_step / 1e3) / 1e9,
         without_signature_output=dict(kernel_ms=nb_ms, algorithmic_bytes=nb_bytes,
                                       achieved_gbs=nb_bytes / (nb_ms / 1e3) / 1e9,
@@ -396,9 +402,10 @@ def bench_stream(args):
         clock_settle=dict(seconds=args.settle, steps=n_settle), ms_per_step=ms_per_step, higher_is_better=True,
         scaling="weak", vs_baseline=None, dtype="i32", data="synthetic",
         config=dict(workload=w["name"], micro_batches=nmb, tokens_per_micro_batch=N, experts=E, k=k,
-                    score_dtype="bf16", buffer_sets=copies),
-        roofline=roofline(alg, kern_ms, w["name"], "k_topk (stream append, 16 micro-batches per launch)",
-                          bytes_per_token),
+                    score_dtype="bf16", buffer_sets=copies, gram=args.gram),
+        roofline=roofline(alg, kern_ms, w["name"], "k_topk (stream append, 16 micro-batches per launch, "
+                          + ("fp4 MFMA Gram)" if args.gram == "mfma" else "popcount Gram)"),
+                          bytes_per_token, args.gram),
         step_gbs=alg / (ms_per_step / 1e3) / 1e9,
         step_frac=alg / (ms_per_step / 1e3) / 1e9 / HBM_PEAK_GBS,
         check=dict(sum=rec["sum"], expected_sum=2 * tokens * k * (E - k)),
@@ -419,6 +426,8 @@ def main():
     import paper_2609_32398_amd as dl
 
     dl.lib()
+    if args.gram == "popc":
+        dl.set_option(dl.DO_OPT_GRAM, 1)
     if args.calibrate_copy:
         n = 1 << 30  # 4 GiB of fp32
         src = torch.ones(n, dtype=torch.float32, device="cuda")
