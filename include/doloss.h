@@ -232,11 +232,13 @@ int64_t do_stream_tokens(const do_stream* h);
 int64_t do_stream_words_per_expert(const do_stream* h);
 
 /*
- * Benchmark hook: the next do_fused / do_topk_signature / do_stream_append*
- * call made by this thread records `start` on its stream right before its
- * main score-streaming kernel and `stop` right after it (one-shot; both are
- * events of the current device created by the caller).  Pass NULLs to
- * cancel.  Lets a caller time that kernel alone with hipEventElapsedTime.
+ * Benchmark hook: the next do_fused / do_topk_signature / do_stream_append* /
+ * do_global_batch_noalloc call made by this thread binds `start` and `stop`
+ * to the dispatch of its main score-streaming kernel (hipExtLaunchKernel), so
+ * that hipEventElapsedTime gives that kernel's own run time.  do_surrogate
+ * records them on its stream right before and after its main kernel.
+ * One-shot; both are events of the current device created by the caller
+ * (either may be NULL).  Pass NULLs to cancel.
  */
 do_status do_profile_next(hipEvent_t start, hipEvent_t stop);
 

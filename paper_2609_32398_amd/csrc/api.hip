@@ -18,6 +18,17 @@ thread_local std::string g_last_error;
 thread_local hipEvent_t g_prof_start = nullptr;
 thread_local hipEvent_t g_prof_stop = nullptr;
 
+// Hands the one-shot profiling events to the Top-K launch `f(pe)`, which binds
+// them to its kernel dispatch.
+template <typename F>
+hipError_t profiled_topk(F&& f) {
+  dol::ProfEv pe;
+  pe.start = g_prof_start;
+  pe.stop = g_prof_stop;
+  g_prof_start = g_prof_stop = nullptr;
+  return f(pe);
+}
+
 // Records the one-shot profiling events around the main kernel launch `f`.
 template <typename F>
 hipError_t profiled(hipStream_t s, F&& f) {
@@ -109,7 +120,9 @@ do_status run_layers(const void* scores, do_dtype dt, int64_t N, int32_t E, int3
       tab.s[i].tok_off = 0;
       tab.s[i].layer = l0 + i;
     }
-    DO_TRY(hip_status(profiled(s, [&] { return dol::launch_topk(dt, tab, nseg, a, fast, s); }), "top-k launch"));
+    DO_TRY(hip_status(
+        profiled_topk([&](const dol::ProfEv& pe) { return dol::launch_topk(dt, tab, nseg, a, fast, s, pe); }),
+        "top-k launch"));
   }
   return DO_OK;
 }
@@ -451,7 +464,9 @@ do_status stream_append(do_stream* h, const void* const* scores, do_dtype dtype,
     tab.s[i].tok_off = h->tokens + (int64_t)i * n;
     tab.s[i].layer = 0;
   }
-  DO_TRY(hip_status(profiled(stream, [&] { return dol::launch_topk(dtype, tab, count, a, fast, stream); }),
+  DO_TRY(hip_status(profiled_topk([&](const dol::ProfEv& pe) {
+                      return dol::launch_topk(dtype, tab, count, a, fast, stream, pe);
+                    }),
                     "stream append"));
   h->tokens += (int64_t)count * n;
   h->hist_dirty = std::max(h->hist_dirty, w_end);
@@ -621,7 +636,9 @@ DOLOSS_API do_status do_global_batch_noalloc(const void* const* scores, do_dtype
     tab.s[i].tok_off = (int64_t)i * n_tokens_each;
     tab.s[i].layer = 0;
   }
-  DO_TRY(hip_status(profiled(stream, [&] { return dol::launch_topk(dtype, tab, count, a, fast, stream); }),
+  DO_TRY(hip_status(profiled_topk([&](const dol::ProfEv& pe) {
+                      return dol::launch_topk(dtype, tab, count, a, fast, stream, pe);
+                    }),
                     "global batch"));
   return hip_status(dol::launch_finalize_split(cacc, D, out, E, fin, stream), "finalize");
 }

@@ -78,9 +78,17 @@ hipError_t launch_fill_u64(u64* p, int64_t n, hipStream_t s);
 // Zeroes words [w0, w0 + nw) of `rows` rows that are ld words apart.
 hipError_t launch_fill_rows(u64* p, int64_t ld, int32_t rows, int64_t w0, int64_t nw, hipStream_t s);
 
+// A caller's timing events for one kernel dispatch (either may be null):
+// bound to the dispatch itself, so their interval is that kernel's run.
+struct ProfEv {
+  hipEvent_t start = nullptr;
+  hipEvent_t stop = nullptr;
+};
+
 // Top-K signatures of `nseg` segments; with a.cacc also the co-occurrence
-// counts of each segment's tokens added into a.cacc (popcount Gram).
-hipError_t launch_topk(do_dtype dt, SegTable& tab, int nseg, const PathArgs& a, bool fast_ok, hipStream_t s);
+// counts of each segment's tokens added into a.cacc.  `pe` times the launch.
+hipError_t launch_topk(do_dtype dt, SegTable& tab, int nseg, const PathArgs& a, bool fast_ok, hipStream_t s,
+                       const ProfEv& pe = ProfEv{});
 
 // Co-occurrence counts of existing signatures: cacc[l][i][j] += popcount(F_i & F_j), i <= j,
 // over the first W words of rows that are ld words apart (layers E * ld words apart).

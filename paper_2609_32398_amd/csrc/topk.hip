@@ -45,6 +45,8 @@
 #include <cstdlib>
 #include <mutex>
 
+#include <hip/hip_ext.h>
+
 #include "common.h"
 
 namespace dol {
@@ -1136,7 +1138,7 @@ struct Sched {
 };
 
 template <typename T, int EP, int GM>
-hipError_t launch_one(const SegTable& tab, const PathArgs& a, bool fast, Sched sc, hipStream_t s) {
+hipError_t launch_one(const SegTable& tab, const PathArgs& a, bool fast, Sched sc, hipStream_t s, const ProfEv& pe) {
   constexpr int EPW = EP < 32 ? 32 : EP;
   auto kern = k_topk<T, EP, GM>;
   const size_t lds = (fast ? (size_t)kStageBytes : 0) + 2 * (size_t)kFusedWaves * EPW * sizeof(u64);
@@ -1154,28 +1156,32 @@ hipError_t launch_one(const SegTable& tab, const PathArgs& a, bool fast, Sched s
   const int64_t gs = sc.xcd ? std::max<int64_t>(blocks / 8, 1) : blocks;
   if (gu <= 0 || gu * gs > per_part) gu = (per_part + gs - 1) / gs;  // contiguous ranges
   const int flags = (fast ? 1 : 0) | (sc.xcd ? 2 : 0);
-  hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kFusedThreads), lds, s, tab, a, flags, (uint32_t)gu);
+  if (pe.start != nullptr || pe.stop != nullptr)  // caller's timing events bound to this dispatch
+    hipExtLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kFusedThreads), lds, s, pe.start, pe.stop, 0u, tab, a,
+                          flags, (uint32_t)gu);
+  else
+    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(kFusedThreads), lds, s, tab, a, flags, (uint32_t)gu);
   return hipGetLastError();
 }
 
 template <typename T, int EP>
-hipError_t launch_gm(const SegTable& tab, const PathArgs& a, bool fast, Sched sc, hipStream_t s) {
-  if (a.cacc == nullptr) return launch_one<T, EP, kGramNone>(tab, a, fast, sc, s);
-  if (gram_mode() == kGramPopc) return launch_one<T, EP, kGramPopc>(tab, a, fast, sc, s);
-  return launch_one<T, EP, kGramMfma>(tab, a, fast, sc, s);
+hipError_t launch_gm(const SegTable& tab, const PathArgs& a, bool fast, Sched sc, hipStream_t s, const ProfEv& pe) {
+  if (a.cacc == nullptr) return launch_one<T, EP, kGramNone>(tab, a, fast, sc, s, pe);
+  if (gram_mode() == kGramPopc) return launch_one<T, EP, kGramPopc>(tab, a, fast, sc, s, pe);
+  return launch_one<T, EP, kGramMfma>(tab, a, fast, sc, s, pe);
 }
 
 template <typename T>
-hipError_t launch_ep(const SegTable& tab, const PathArgs& a, bool fast, Sched sc, hipStream_t s) {
+hipError_t launch_ep(const SegTable& tab, const PathArgs& a, bool fast, Sched sc, hipStream_t s, const ProfEv& pe) {
   const int E = a.E;
-  if (E <= 32) return launch_gm<T, 32>(tab, a, fast, sc, s);
-  if (E <= 64) return launch_gm<T, 64>(tab, a, fast, sc, s);
-  if (E <= 128) return launch_gm<T, 128>(tab, a, fast, sc, s);
-  if (E <= 256) return launch_gm<T, 256>(tab, a, fast, sc, s);
+  if (E <= 32) return launch_gm<T, 32>(tab, a, fast, sc, s, pe);
+  if (E <= 64) return launch_gm<T, 64>(tab, a, fast, sc, s, pe);
+  if (E <= 128) return launch_gm<T, 128>(tab, a, fast, sc, s, pe);
+  if (E <= 256) return launch_gm<T, 256>(tab, a, fast, sc, s, pe);
   // E in (256, 1024]: exact per-lane selection, signatures only
   if (a.cacc != nullptr) return hipErrorInvalidValue;
-  if (E <= 512) return launch_one<T, 512, kGramNone>(tab, a, false, sc, s);
-  return launch_one<T, 1024, kGramNone>(tab, a, false, sc, s);
+  if (E <= 512) return launch_one<T, 512, kGramNone>(tab, a, false, sc, s, pe);
+  return launch_one<T, 1024, kGramNone>(tab, a, false, sc, s, pe);
 }
 
 // Launch-time choice of the unit schedule for large launches.  The cost of
@@ -1393,7 +1399,8 @@ __global__ __launch_bounds__(kFusedThreads) void k_gram_mfma(const u64* bits, in
 
 }  // namespace
 
-hipError_t launch_topk(do_dtype dt, SegTable& tab, int nseg, const PathArgs& a, bool fast_ok, hipStream_t s) {
+hipError_t launch_topk(do_dtype dt, SegTable& tab, int nseg, const PathArgs& a, bool fast_ok, hipStream_t s,
+                       const ProfEv& pe) {
   tab.nseg = nseg;
   tab.tile_start[0] = 0;
   for (int i = 0; i < nseg; ++i) {
@@ -1401,7 +1408,13 @@ hipError_t launch_topk(do_dtype dt, SegTable& tab, int nseg, const PathArgs& a, 
     const int64_t words = n > 0 ? ((off + n - 1) >> 6) - (off >> 6) + 1 : 0;
     tab.tile_start[i + 1] = tab.tile_start[i] + (words + kFusedWaves - 1) / kFusedWaves;  // 8-word units
   }
-  if (tab.tile_start[nseg] == 0) return hipSuccess;
+  if (tab.tile_start[nseg] == 0) {  // nothing to launch: the timing events still complete, back to back
+    if (pe.start != nullptr) {
+      const hipError_t e = hipEventRecord(pe.start, s);
+      if (e != hipSuccess) return e;
+    }
+    return pe.stop != nullptr ? hipEventRecord(pe.stop, s) : hipSuccess;
+  }
   const bool fast = fast_ok && a.k <= kFastMaxK && a.E <= kFastMaxE;
   hipEvent_t ev[2] = {nullptr, nullptr};
   const int forced = g_opt_sched.load(std::memory_order_relaxed);
@@ -1410,7 +1423,8 @@ hipError_t launch_topk(do_dtype dt, SegTable& tab, int nseg, const PathArgs& a, 
     const hipError_t e = hipEventRecord(ev[0], s);
     if (e != hipSuccess) return e;
   }
-  const hipError_t e = dt == DO_F32 ? launch_ep<float>(tab, a, fast, sc, s) : launch_ep<uint16_t>(tab, a, fast, sc, s);
+  const hipError_t e =
+      dt == DO_F32 ? launch_ep<float>(tab, a, fast, sc, s, pe) : launch_ep<uint16_t>(tab, a, fast, sc, s, pe);
   if (e != hipSuccess || ev[1] == nullptr) return e;
   return hipEventRecord(ev[1], s);
 }
