@@ -316,6 +316,58 @@ __device__ void exact_topk_passes_lane(const T* row, int E, int k, u64* bt, int 
   }
 }
 
+// Exact selection of one lane's token (the paths above), kept out of line:
+// inlined into the Top-K kernel, its registers and live ranges cost the
+// kernel's common path spills although it runs for few tokens.
+template <typename T>
+__device__ __attribute__((noinline)) void exact_select_lane(const T* row, int E, int k, u64* bt, int swz, u64 bit) {
+  if (k <= 8)
+    exact_topk_list_lane<T, 8>(row, E, k, bt, swz, bit);
+  else if (k <= 16)
+    exact_topk_list_lane<T, 16>(row, E, k, bt, swz, bit);
+  else
+    exact_topk_passes_lane<T>(row, E, k, bt, swz, bit);
+}
+
+// Tokens whose k-th and (k+1)-th fp32 keys share a 24-bit value bucket
+// (bit L of tie_mask; B = bucket of sk, need = picks still missing; row0 =
+// the row of lane 0's token; swz = the wave's bit-tile swizzle).  For each,
+// the whole wave loads the token's row (16 bytes per lane, one round trip),
+// marks the elements of the bucket with a 16-bit sub-key (low 8 value bits,
+// then the complemented index) and takes the `need` largest across the wave:
+// by full value, ties to the lower index.  Out of line for the same reason as
+// exact_select_lane; every lane of the wave must be active.
+__device__ __attribute__((noinline)) void resolve_ties(u64 tie_mask, int sk_v, int need_v, bool gen_keys, u64* mybt,
+                                                      const unsigned char* row0, int rowB, int swz) {
+  const int lane = (int)__lane_id();
+  while (tie_mask != 0ull) {
+    const int L = __builtin_ctzll(tie_mask);
+    tie_mask &= tie_mask - 1;
+    const int B = __builtin_amdgcn_readlane(sk_v, L) >> 8;
+    const int need_l = __builtin_amdgcn_readlane(need_v, L);
+    const unsigned char* row = row0 + (int64_t)L * rowB;
+    const bool has = lane * 16 < rowB;
+    const v4u x = has ? *reinterpret_cast<const v4u*>(row + lane * 16) : v4u{0u, 0u, 0u, 0u};
+    int sub[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      uint32_t u = x[j];
+      if (gen_keys) u ^= (uint32_t)((int32_t)u >> 31) & 0x7FFFFFFFu;
+      const int e = lane * 4 + j;
+      sub[j] = (has && ((int32_t)u >> 8) == B) ? (int)(((u & 0xFFu) << 8) | (uint32_t)(255 - e)) : -1;
+    }
+    for (int r = 0; r < need_l; ++r) {
+      int m = max(max(sub[0], sub[1]), max(sub[2], sub[3]));
+#pragma unroll
+      for (int d = 1; d < kWave; d <<= 1) m = max(m, __shfl_xor(m, d));
+      if (m < 0) break;
+      if (lane == 0) atomicOr(&mybt[(255 - (m & 255)) ^ swz], 1ull << L);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) sub[j] = (sub[j] == m) ? -1 : sub[j];
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Popcount Gram held in registers across a block: thread `tid` owns up to MTQ
 // 4x4 micro-tiles (a, b), a <= b, of the upper triangle of c.
@@ -780,42 +832,6 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
     }
   };
 
-  // Tokens whose k-th and (k+1)-th fp32 keys share a 24-bit value bucket
-  // (bit L of tie_mask; B = bucket of sk, need = picks still missing; row0 =
-  // the row of lane 0's token).  For
-  // each, the whole wave loads the token's row (16 bytes per lane, one round
-  // trip), marks the elements of the bucket with a 16-bit sub-key (low 8 value
-  // bits, then the complemented index) and takes the `need` largest across the
-  // wave: by full value, ties to the lower index.
-  auto resolve_ties = [&](u64 tie_mask, int sk_v, int need_v, bool gen_keys, u64* mybt_, const unsigned char* row0) {
-    while (tie_mask != 0ull) {
-      const int L = __builtin_ctzll(tie_mask);
-      tie_mask &= tie_mask - 1;
-      const int B = __builtin_amdgcn_readlane(sk_v, L) >> 8;
-      const int need_l = __builtin_amdgcn_readlane(need_v, L);
-      const unsigned char* row = row0 + (int64_t)L * rowB;
-      const bool has = lane * 16 < rowB;
-      const v4u x = has ? *reinterpret_cast<const v4u*>(row + lane * 16) : v4u{0u, 0u, 0u, 0u};
-      int sub[4];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        uint32_t u = x[j];
-        if (gen_keys) u ^= (uint32_t)((int32_t)u >> 31) & 0x7FFFFFFFu;
-        const int e = lane * 4 + j;
-        sub[j] = (has && ((int32_t)u >> 8) == B) ? (int)(((u & 0xFFu) << 8) | (uint32_t)(255 - e)) : -1;
-      }
-      for (int r = 0; r < need_l; ++r) {
-        int m = max(max(sub[0], sub[1]), max(sub[2], sub[3]));
-#pragma unroll
-        for (int d = 1; d < kWave; d <<= 1) m = max(m, __shfl_xor(m, d));
-        if (m < 0) break;
-        if (lane == 0) atomicOr(&mybt_[(255 - (m & 255)) ^ bt_swz(wave)], 1ull << L);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) sub[j] = (sub[j] == m) ? -1 : sub[j];
-      }
-    }
-  };
-
   constexpr int kGramStep = GM == kGramMfma ? Mfma<GS::TS>::kWords : 1;  // slots per Gram step
   constexpr int kMaxAccUnits = ((1 << 24) / 512) - 1;  // units per flush at most (counts < 2^24)
   int acc_units = 0;
@@ -1078,19 +1094,14 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
         }
         if (!Traits<T>::kExact) {
           const u64 tm = __ballot(tie);
-          if (tm != 0ull) resolve_ties(tm, sk, need, gen, mybt, word_rows(sv, wl, rowB));
+          if (tm != 0ull) resolve_ties(tm, sk, need, gen, mybt, word_rows(sv, wl, rowB), rowB, bt_swz(wave));
         }
         if (__ballot(nonpos) != 0ull) gen = true;
       }
       if (__ballot(need_slow) != 0ull) {
         if (need_slow) {
           const T* rp = reinterpret_cast<const T*>(word_rows(sv, wl, rowB) + (uint32_t)lane * (uint32_t)rowB);
-          if (k <= 8)
-            exact_topk_list_lane<T, 8>(rp, E, k, mybt, bt_swz(wave), 1ull << lane);
-          else if (k <= 16)
-            exact_topk_list_lane<T, 16>(rp, E, k, mybt, bt_swz(wave), 1ull << lane);
-          else
-            exact_topk_passes_lane<T>(rp, E, k, mybt, bt_swz(wave), 1ull << lane);
+          exact_select_lane<T>(rp, E, k, mybt, bt_swz(wave), 1ull << lane);
         }
       }
     }
