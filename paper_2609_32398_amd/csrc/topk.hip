@@ -638,6 +638,18 @@ __device__ __forceinline__ void mfma_flush(const typename Mfma<TS>::Acc (&acc)[k
   }
 }
 
+// The flush of the Top-K kernel, out of line: it runs a few times per block,
+// and inlined, its address arithmetic and atomics cost the kernel's unit loop
+// registers (SGPR and VGPR spills).  The accumulators travel by value.
+template <int TS>
+__device__ __attribute__((noinline)) void mfma_flush_ool(typename Mfma<TS>::Acc a0, typename Mfma<TS>::Acc a1,
+                                                         typename Mfma<TS>::Acc a2, typename Mfma<TS>::Acc a3,
+                                                         typename Mfma<TS>::Acc a4, WaveTiles wt, uint32_t* c, int E,
+                                                         int rot, bool pair64) {
+  const typename Mfma<TS>::Acc acc[kGP] = {a0, a1, a2, a3, a4};
+  mfma_flush<TS>(acc, wt, c, E, (int)__lane_id(), rot, pair64);
+}
+
 #define DOL_WAVE_FENCE() asm volatile("" ::: "memory")
 
 // One segment as the kernel sees it (all values wave-uniform).  Counts fit
@@ -944,7 +956,7 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
     uint32_t* cl = a.cacc + (int64_t)layer * a.cacc_layer_elems +
                    (a.ncopies > 1 ? (int64_t)(blockIdx.x % (uint32_t)a.ncopies) * a.cacc_copy_elems : 0);
     if (GM == kGramMfma) {
-      mfma_flush<GS::TS>(acc, wt, cl, E, lane, (int)(blockIdx.x % kGP), pair64);
+      mfma_flush_ool<GS::TS>(acc[0], acc[1], acc[2], acc[3], acc[4], wt, cl, E, (int)(blockIdx.x % kGP), pair64);
       zero_acc();
     }
     if (GM == kGramPopc) {
