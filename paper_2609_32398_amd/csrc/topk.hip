@@ -719,8 +719,13 @@ typedef unsigned long long v2u64 __attribute__((ext_vector_type(2)));
 // rows, k <= 8, E <= 256); bit 1: XCD-partitioned schedule.  gu: units per
 // schedule group.
 // ---------------------------------------------------------------------------
-template <typename T, int EP, int GM>
+template <typename T, int EP, int GM, bool AL>
 __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, const PathArgs a, int flags, uint32_t gu) {
+  // AL: every segment starts and ends on a unit boundary (token offset and
+  // count multiples of 512) and rows are whole 128-byte chunks, so every word
+  // is full, every unit has 8 words, no word is shared between segments and
+  // every row of a chunk lies inside its segment.  The edge handling then
+  // compiles away, with the registers it holds.
   (void)tab_arg;  // read through `tab` below (it is the first kernel argument)
   const SegTablePtr tab = (SegTablePtr)__builtin_amdgcn_kernarg_segment_ptr();
   constexpr int EPW = EP < 32 ? 32 : EP;  // signature words per slot of the bit tile
@@ -806,7 +811,7 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
   auto dma = [&](const Seg& sg, uint32_t wl, int c_, unsigned char* sbuf) {
     if (c_ * 8 + 8 > rowv) return;
     const unsigned char* cbase = word_rows(sg, wl, rowB) + c_ * 128;  // row 0 of the chunk (uniform)
-    if (wl >= sg.full_lo && wl < sg.full_hi) {  // every row inside the segment
+    if (AL || (wl >= sg.full_lo && wl < sg.full_hi)) {  // every row inside the segment
       const __amdgpu_buffer_rsrc_t rs =
           __builtin_amdgcn_make_buffer_rsrc(const_cast<unsigned char*>(cbase), (short)0, 0x7FFFFFFF, kBufWord3);
 #pragma unroll
@@ -892,7 +897,9 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
   auto store_share = [&](const u64* pbt) __attribute__((always_inline)) {
     if (pend.lb == nullptr) return;
     const int e_lo = (wave * E) >> 3, e_hi = ((wave + 1) * E) >> 3;
-    if (EPW <= 256 && (pend.w0 & 1) == 0 && pend.cnt == kFusedWaves && !pend.shared_lo && pend.shared_hi < 0) {
+    const bool plain_unit =
+        AL || ((pend.w0 & 1) == 0 && pend.cnt == kFusedWaves && !pend.shared_lo && pend.shared_hi < 0);
+    if (EPW <= 256 && plain_unit) {
       if (sb_n > 0 && (sb_lb != pend.lb || sb_w0 + 8 * sb_n != pend.w0)) batch_flush();
       if (sb_n == 0) {
         sb_lb = pend.lb;
@@ -994,7 +1001,7 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
   int buf = 0;
   for (uint32_t u = ug; u < U; buf ^= 1) {
     const uint32_t wl = tl0 + wave;                      // this wave's local word
-    const int cnt = (int)min((uint32_t)kFusedWaves, sv.words - tl0);  // words in this unit
+    const int cnt = AL ? kFusedWaves : (int)min((uint32_t)kFusedWaves, sv.words - tl0);  // words in this unit
     // next unit and its segment (wave-uniform)
     const uint32_t un = next_unit(u);
     int seg_n = seg;
@@ -1008,7 +1015,7 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
       tl0n = 8 * (un - svn.u_begin);
     }
     const uint32_t wln = tl0n + wave;
-    const bool next_mine = un < U && wln < svn.words;
+    const bool next_mine = un < U && (AL || wln < svn.words);
 
     u64* bt = bt_all + buf * kFusedWaves * EPW;
     const u64* pbt = bt_all + (buf ^ 1) * kFusedWaves * EPW;  // the pending unit's tile
@@ -1019,15 +1026,15 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
     DOL_WAVE_FENCE();
     int gram_done = have_pend ? 0 : kFusedWaves;  // slots of the pending unit already accumulated
     bool stored = !have_pend;
-    if (fast && wave >= cnt && next_mine) {
+    if (!AL && fast && wave >= cnt && next_mine) {
       // idle in this unit (segment end) but busy in the next one: start that
       // word's first chunk now, into the buffer the next unit reads first
       dma(svn, wln, 0, st + cb * kChunkBytes);
     }
-    if (wave < cnt) {
+    if (AL || wave < cnt) {
       // the lane's row holds a token of the segment (every row of an interior word does)
       const uint32_t row = (wl << 6) + (uint32_t)lane;
-      const bool valid = (wl >= sv.full_lo && wl < sv.full_hi) ||
+      const bool valid = AL || (wl >= sv.full_lo && wl < sv.full_hi) ||
                          (row >= sv.sh && (uint64_t)row < (uint64_t)sv.sh + (uint64_t)sv.n);
       bool need_slow = valid;
       if (fast) {
@@ -1037,7 +1044,7 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
         for (int i = 0; i < 8; ++i) top[i] = INT_MIN;
         for (int c = 0; c < nch; ++c) {
           unsigned char* cur = st + cb * kChunkBytes;
-          if (c * 8 + 8 <= rowv) {
+          if (AL || c * 8 + 8 <= rowv) {
             DOL_WAIT_VMEM();  // this chunk's direct-to-LDS loads (and earlier stores) have completed
           } else {
             fill_partial(sv, wl, c, cur);
@@ -1131,8 +1138,8 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
     pend.w0 = sv.w_first + tl0;
     pend.cnt = cnt;
     pend.layer = sv.layer;
-    pend.shared_lo = a.or_partial && tl0 == 0 && sv.sh != 0;
-    pend.shared_hi = (a.or_partial && tl0 + cnt == sv.words && ((sv.sh + sv.n) & 63) != 0) ? cnt - 1 : -1;
+    pend.shared_lo = !AL && a.or_partial && tl0 == 0 && sv.sh != 0;
+    pend.shared_hi = (!AL && a.or_partial && tl0 + cnt == sv.words && ((sv.sh + sv.n) & 63) != 0) ? cnt - 1 : -1;
     have_pend = true;
     u = un;
     seg = seg_n;
@@ -1160,10 +1167,10 @@ struct Sched {
   bool xcd;
 };
 
-template <typename T, int EP, int GM>
+template <typename T, int EP, int GM, bool AL = false>
 hipError_t launch_one(const SegTable& tab, const PathArgs& a, bool fast, Sched sc, hipStream_t s, const ProfEv& pe) {
   constexpr int EPW = EP < 32 ? 32 : EP;
-  auto kern = k_topk<T, EP, GM>;
+  auto kern = k_topk<T, EP, GM, AL>;
   const size_t lds = (fast ? (size_t)kStageBytes : 0) + 2 * (size_t)kFusedWaves * EPW * sizeof(u64);
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -1187,8 +1194,26 @@ hipError_t launch_one(const SegTable& tab, const PathArgs& a, bool fast, Sched s
   return hipGetLastError();
 }
 
+// Segments on unit boundaries with rows of whole 128-byte chunks (the
+// condition of k_topk's AL specialization).
+bool aligned_segments(const SegTable& tab, int rowB) {
+  if (rowB % 128 != 0) return false;
+  for (int i = 0; i < tab.nseg; ++i)
+    if (tab.s[i].n % 512 != 0 || tab.s[i].tok_off % 512 != 0) return false;
+  return true;
+}
+
 template <typename T, int EP>
 hipError_t launch_gm(const SegTable& tab, const PathArgs& a, bool fast, Sched sc, hipStream_t s, const ProfEv& pe) {
+  // the aligned specialization pays off up to 128 experts (bf16 workloads:
+  // -11 %); at 256 fp32 experts it measured 1 % slower, so it is not built there
+  if constexpr (EP <= 128) {
+    if (fast && aligned_segments(tab, a.E * (int)sizeof(T))) {
+      if (a.cacc == nullptr) return launch_one<T, EP, kGramNone, true>(tab, a, fast, sc, s, pe);
+      if (gram_mode() == kGramPopc) return launch_one<T, EP, kGramPopc, true>(tab, a, fast, sc, s, pe);
+      return launch_one<T, EP, kGramMfma, true>(tab, a, fast, sc, s, pe);
+    }
+  }
   if (a.cacc == nullptr) return launch_one<T, EP, kGramNone>(tab, a, fast, sc, s, pe);
   if (gram_mode() == kGramPopc) return launch_one<T, EP, kGramPopc>(tab, a, fast, sc, s, pe);
   return launch_one<T, EP, kGramMfma>(tab, a, fast, sc, s, pe);

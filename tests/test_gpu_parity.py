@@ -84,6 +84,50 @@ def test_random_shapes_normal(dl, orc, syn, E, k, N, dtype):
     _run_all_entry_points(dl, orc, x, k, f"normal E={E} k={k} N={N}")
 
 
+# Unit-aligned launches (token counts and offsets multiples of 512, rows of
+# whole 128-byte chunks) run a specialization of the score pass up to 128
+# experts: fp32 rows of 32, 64, 96, 128 experts, bf16 rows of 64 and 128;
+# several layers, every entry point, normal and tie-heavy scores.
+@pytest.mark.parametrize("E,k,N,dtype", [(32, 1, 512, 0), (64, 8, 1536, 0), (96, 5, 2048, 0), (128, 8, 4608, 0),
+                                         (64, 6, 512, 1), (128, 8, 3584, 1), (128, 1, 1024, 1)])
+def test_unit_aligned_layers(dl, orc, syn, E, k, N, dtype):
+    x = syn.normal(4000 + E + N, N, E, dtype)
+    _run_all_entry_points(dl, orc, x, k, f"aligned normal E={E} k={k} N={N}")
+    t = syn.int_ties(4100 + E, N, E, -3, 3, dtype)
+    _run_all_entry_points(dl, orc, t, k, f"aligned ties E={E} k={k} N={N}")
+    print(f"[case] aligned 3 layers E={E} k={k} N={N}", flush=True)
+    layers = [syn.normal(4200 + E + l, N, E, dtype) for l in range(3)]
+    xd = to_dev(np.stack(layers))
+    bits, D, out = dl.do_fused(xd, k, want_bits=True)
+    torch.cuda.synchronize()
+    recs = dl.loss_records(out)
+    for l, xl in enumerate(layers):
+        _check_layer(dl, orc, xl, k, bits[l], D[l], recs[l], f"aligned layer {l}")
+
+
+@pytest.mark.parametrize("E,k,dtype", [(128, 8, 1), (64, 6, 0)])
+def test_stream_unit_aligned_and_unaligned_appends(dl, orc, syn, E, k, dtype):
+    # aligned appends (the specialization), then an unaligned one, then
+    # aligned again at an unaligned offset (the general kernel), one history
+    print(f"[case] stream aligned/unaligned E={E} k={k} dtype={dtype}", flush=True)
+    sizes = [2048, 512, 512, 1000, 512, 1536]
+    parts = [syn.normal(4300 + i, n, E, dtype) for i, n in enumerate(sizes)]
+    s = dl.DoStream(E, k, sum(sizes))
+    s.append(to_dev(parts[0]))
+    s.append_many([to_dev(parts[1]), to_dev(parts[2])])
+    s.append(to_dev(parts[3]))
+    s.append_many([to_dev(parts[4])])
+    s.append(to_dev(parts[5]))
+    D, out = s.finalize()
+    hist = s.history()
+    torch.cuda.synchronize()
+    F, words, ref_D, ref_L = orc.run_stream(parts, k)
+    np.testing.assert_array_equal(D_np(D), ref_D)
+    loss_close(dl.loss_records(out)[0], ref_L)
+    np.testing.assert_array_equal(bits_np(hist)[:, : words.shape[1]], words)
+    s.close()
+
+
 @pytest.mark.parametrize("E,k,N", [(8, 2, 500), (24, 8, 700), (64, 6, 999), (128, 8, 1500), (256, 8, 640),
                                    (40, 3, 128), (96, 8, 200)])
 @pytest.mark.parametrize("dtype", [0, 1])
