@@ -793,6 +793,18 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
   const int q_even = (lane & 7) ^ (lane >> 3);
   const uint32_t off_even = (uint32_t)((lane >> 3) * rowB + q_even * 16);        // bytes from the chunk's row 0
   const uint32_t off_odd = (uint32_t)((lane >> 3) * rowB + (q_even ^ 1) * 16);  // odd j: piece q_even ^ 1
+  // Up to 128 experts the lane offsets of the eight loads of a full chunk are
+  // kept in VGPRs: as scalar offsets they are spilled and read back (with
+  // hazard waits) per load (-1 % at the stream workload).  At 256 experts the
+  // VGPRs are full and the scalar offsets measured faster.
+  constexpr bool kVoff = EP <= 128;
+  uint32_t voff[8] = {};
+  if constexpr (kVoff) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) voff[j] = ((j & 1) ? off_odd : off_even) + (uint32_t)(j * 8 * rowB);
+    asm volatile("" : "+v"(voff[0]), "+v"(voff[1]), "+v"(voff[2]), "+v"(voff[3]), "+v"(voff[4]), "+v"(voff[5]),
+                 "+v"(voff[6]), "+v"(voff[7]));
+  }
 
   // Rows [r_lo, r_hi) of local word wl of segment sg hold its tokens
   // (wave-uniform; 64-bit only where sh + n may reach 2^32).
@@ -816,9 +828,13 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
           __builtin_amdgcn_make_buffer_rsrc(const_cast<unsigned char*>(cbase), (short)0, 0x7FFFFFFF, kBufWord3);
 #pragma unroll
       for (int j = 0; j < 8; ++j)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)(sbuf + j * 1024), 16,
-                                                 (j & 1) ? off_odd : off_even, (uint32_t)(j * 8 * rowB), 0,
-                                                 kStreamPolicy);
+        if constexpr (kVoff)
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)(sbuf + j * 1024), 16,
+                                                   voff[j], 0, 0, kStreamPolicy);
+        else
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)(sbuf + j * 1024), 16,
+                                                   (j & 1) ? off_odd : off_even, (uint32_t)(j * 8 * rowB), 0,
+                                                   kStreamPolicy);
     } else {
       int r_lo, r_hi;
       row_bounds(sg, wl, r_lo, r_hi);
