@@ -476,12 +476,15 @@ class DoStream:
                "do_stream_append_many")
 
     def finalize(self, D: torch.Tensor | None = None, out: torch.Tensor | None = None):
+        # the caller's buffers are checked before any is allocated
+        if D is not None:
+            _want(D, "D", numel=self.E * self.E, dtypes=_I32)
+        if out is not None:
+            _want(out, "out", numel=LOSS_RESULT_BYTES, dtypes=_U8)
         if D is None:
             D = torch.empty((self.E, self.E), dtype=torch.int32, device=torch.cuda.current_device())
         if out is None:
             out = alloc_out(1, torch.device("cuda", torch.cuda.current_device()))
-        _want(D, "D", numel=self.E * self.E, dtypes=_I32)
-        _want(out, "out", numel=LOSS_RESULT_BYTES, dtypes=_U8)
         _check(lib().do_stream_finalize(self.h, D.data_ptr(), out.data_ptr(), _stream()), "do_stream_finalize")
         return D, out
 

@@ -234,6 +234,8 @@ def test_stream_binding_rejects_bad_micro_batches(host_binding):
         s.append_many([])
     with pytest.raises(ValueError):
         s.finalize(torch.zeros(15, 15, dtype=torch.int32), torch.zeros(1, 40, dtype=torch.uint8))
+    with pytest.raises(ValueError):
+        s.finalize(torch.zeros(16, 16, dtype=torch.float32))  # D not int32, checked before `out` is allocated
 
 
 def test_set_option_rejects_unknown_values(dl):
