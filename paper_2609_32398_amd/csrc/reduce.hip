@@ -267,12 +267,18 @@ __global__ __launch_bounds__(1024) void k_finalize(const uint32_t* cacc, uint32_
 
 constexpr int kSplitRows = 8;  // rows per block of the split finalize, one per wave
 
+// Before a block's ticket: wait until this thread's atomics on the sums are
+// performed.  The block that takes the last ticket reads the sums with
+// atomics, so it needs no cache writeback from the others; an agent-scope
+// fence (__threadfence) would write back the whole L2 in every block.
+__device__ __forceinline__ void fin_wait() { __builtin_amdgcn_s_waitcnt(0); }
+
 // The finalize of one layer over ceil(E/8) blocks of 512 threads (E <= 256),
 // for a single layer where one block would leave the GPU idle: wave w of
 // block b owns row 8b + w.  Every block adds its exact (S1, S2) into fin[0],
 // fin[1] and takes a ticket from fin[2]; the block with the last ticket
 // writes the loss record and clears fin for the next call.  All accesses to
-// fin are atomics.  c must not alias D.
+// fin are atomics (the ticket needs no fence, see fin_wait).  c must not alias D.
 __global__ __launch_bounds__(512) void k_finalize_split(const uint32_t* __restrict__ c, uint32_t* __restrict__ d,
                                                         do_loss_result* out, int E, u64* fin) {
   __shared__ uint32_t diag[kFastMaxE];
@@ -307,9 +313,8 @@ __global__ __launch_bounds__(512) void k_finalize_split(const uint32_t* __restri
   if (threadIdx.x == 0) {
     atomicAdd(&fin[0], s1);
     atomicAdd(&fin[1], s2);
-    __threadfence();
+    fin_wait();
     if (atomicAdd(&fin[2], 1ull) == (u64)gridDim.x - 1) {
-      __threadfence();
       const u64 S1 = atomicAdd(&fin[0], 0ull), S2 = atomicAdd(&fin[1], 0ull);
       write_result(out, S1, 0ull, S2, E);
       atomicExch(&fin[0], 0ull);
@@ -409,13 +414,13 @@ __global__ __launch_bounds__(512) void k_finalize_stream(uint32_t* copies, int n
   if (threadIdx.x == 0) {
     atomicAdd(&fin[0], s1);
     atomicAdd(&fin[1], s2);
-    __threadfence();
+    fin_wait();
     last = atomicAdd(&fin[2], 1ull) == (u64)gridDim.x - 1;
   }
   __syncthreads();
   if (!last) return;
-  // every block has read the diagonal: move it into the snapshot
-  __threadfence();
+  // every block has read the diagonal (its loads returned before its ticket):
+  // move it into the snapshot
   for (int j = threadIdx.x; j < E; j += blockDim.x) {
     const int64_t o = (int64_t)j * E + j;
     snap[o] = diag[j];
