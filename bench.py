@@ -228,15 +228,20 @@ def bench_layers(args, cfg):
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
     t_start.record()
-    for a, b in ks:
-        dl.do_profile_next(a, b)
+    for _ in range(args.steps):
         step()
     t_stop.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     total_ms = t_start.elapsed_time(t_stop)
-    kern_ms = sum(a.elapsed_time(b) for a, b in ks) / len(ks)
     ms_per_step = total_ms / args.steps
+    # the Top-K kernel's own duration: the same steps again, each with a pair
+    # of events bound to its dispatch (the binding costs a few us per step)
+    for a, b in ks:
+        dl.do_profile_next(a, b)
+        step()
+    torch.cuda.synchronize()
+    kern_ms = sum(a.elapsed_time(b) for a, b in ks) / len(ks)
     tokens = L * N
     elem = 4 if w["dtype"] == 0 else 2
     bytes_per_token = E * elem + E // 8
@@ -381,14 +386,19 @@ def bench_stream(args):
     t_stop = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t_start.record()
+    for i in range(args.steps):
+        step(i)
+    t_stop.record()
+    torch.cuda.synchronize()
+    ms_per_step = t_start.elapsed_time(t_stop) / args.steps
+    # the append kernel's own duration: the same steps again, with a pair of
+    # events bound to each append's dispatch (the binding costs a few us per step)
     for i, (a, b) in enumerate(ks):
         s.reset()
         dl.do_profile_next(a, b)
         s.append_many(bufs[i % copies])
         s.finalize(D, out)
-    t_stop.record()
     torch.cuda.synchronize()
-    ms_per_step = t_start.elapsed_time(t_stop) / args.steps
     kern_ms = sum(a.elapsed_time(b) for a, b in ks) / len(ks)
     tokens = nmb * N
     bytes_per_token = E * 2 + E // 8
