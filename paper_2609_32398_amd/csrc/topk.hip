@@ -1252,17 +1252,19 @@ hipError_t launch_ep(const SegTable& tab, const PathArgs& a, bool fast, Sched sc
 // the signature stores under a given schedule differs between otherwise
 // identical boards (it follows how the concurrent store streams fall on
 // the HBM channels), while it repeats within one process.  So for each
-// large launch shape the first launches try the candidates with events
-// around them; completed measurements are collected with hipEventQuery,
-// which never waits, and once every candidate has one, the fastest is used
-// for all later launches of that shape.  The very first launch of a shape is
-// not measured (cold caches and TLB).  Launches under stream capture and
+// large launch shape the first launches try the candidates in turn with
+// events around them; completed measurements are collected with
+// hipEventQuery, which never waits, and once every candidate has kTuneTrials
+// of them, the one with the fastest launch is used for all later launches of
+// that shape (it must beat the first candidate by 2 %).  The very first
+// launch of a shape is not measured (cold caches and TLB).  Launches under stream capture and
 // launches below kTuneMinUnits use the first candidate (or the one already
 // chosen for the shape); a capture never touches the measurement events.
 // When every slot of the table holds a shape, a decided one is recycled.
 constexpr Sched kSchedCand[2] = {Sched{4, true}, Sched{0, false}};  // XCD partitions; contiguous ranges
 constexpr int kNumCand = 2;
-constexpr int64_t kTuneMinUnits = 8192;  // 4 Mi tokens
+constexpr int64_t kTuneMinUnits = 1024;  // 512 Ki tokens
+constexpr int kTuneTrials = 3;           // measured launches per candidate
 constexpr int kTuneSlots = 16;
 
 struct Tune {
@@ -1271,6 +1273,7 @@ struct Tune {
   int calls;
   int chosen;                 // index into kSchedCand, or -1 while measuring
   float best[kNumCand];       // fastest completed launch per candidate (ms), < 0 if none yet
+  int trials[kNumCand];       // completed measurements per candidate
   bool pending[kNumCand];     // a measured launch is in flight
   hipEvent_t ev[kNumCand][2];
 };
@@ -1350,8 +1353,10 @@ Sched tuned_schedule(do_dtype dt, const SegTable& tab, const PathArgs& a, bool f
       const hipError_t q = hipEventQuery(t->ev[c][1]);
       if (q == hipSuccess) {
         float ms = -1.f;
-        if (hipEventElapsedTime(&ms, t->ev[c][0], t->ev[c][1]) == hipSuccess && ms > 0.f)
+        if (hipEventElapsedTime(&ms, t->ev[c][0], t->ev[c][1]) == hipSuccess && ms > 0.f) {
           t->best[c] = t->best[c] < 0.f ? ms : std::min(t->best[c], ms);
+          ++t->trials[c];
+        }
         t->pending[c] = false;
       } else if (q != hipErrorNotReady) {
         t->pending[c] = false;
@@ -1359,12 +1364,12 @@ Sched tuned_schedule(do_dtype dt, const SegTable& tab, const PathArgs& a, bool f
         return kSchedCand[0];
       }
     }
-    all = all && t->best[c] > 0.f;
+    all = all && t->trials[c] >= kTuneTrials;
   }
   if (all) {
     int bc = 0;
     for (int c = 1; c < kNumCand; ++c)
-      if (t->best[c] < 0.97f * t->best[bc]) bc = c;  // switch only for a clear gain
+      if (t->best[c] < 0.98f * t->best[bc]) bc = c;  // switch only for a clear gain
     if (getenv("DOLOSS_TUNE_LOG") != nullptr)
       fprintf(stderr, "[doloss] unit schedule for %lld units: candidates %.4f / %.4f ms, chose %d\n",
               (long long)units, t->best[0], t->best[1], bc);
@@ -1372,20 +1377,25 @@ Sched tuned_schedule(do_dtype dt, const SegTable& tab, const PathArgs& a, bool f
     return kSchedCand[bc];
   }
   if (t->calls++ == 0) return kSchedCand[0];
-  for (int c = 0; c < kNumCand; ++c) {
-    if (t->best[c] > 0.f || t->pending[c]) continue;
-    if (t->ev[c][0] == nullptr) {
-      if (hipEventCreate(&t->ev[c][0]) != hipSuccess || hipEventCreate(&t->ev[c][1]) != hipSuccess) {
-        decide(*t, 0);
-        return kSchedCand[0];
-      }
-    }
-    t->pending[c] = true;
-    ev_out[0] = t->ev[c][0];
-    ev_out[1] = t->ev[c][1];
-    return kSchedCand[c];
+  // the candidate with the fewest measurements that has none in flight
+  // (ties to the one measured least recently, so the candidates alternate)
+  int pick = -1;
+  for (int i = 0; i < kNumCand; ++i) {
+    const int c = (t->calls + i) % kNumCand;
+    if (t->pending[c] || t->trials[c] >= kTuneTrials) continue;
+    if (pick < 0 || t->trials[c] < t->trials[pick]) pick = c;
   }
-  return kSchedCand[0];
+  if (pick < 0) return kSchedCand[0];  // every candidate still has a launch in flight
+  if (t->ev[pick][0] == nullptr) {
+    if (hipEventCreate(&t->ev[pick][0]) != hipSuccess || hipEventCreate(&t->ev[pick][1]) != hipSuccess) {
+      decide(*t, 0);
+      return kSchedCand[0];
+    }
+  }
+  t->pending[pick] = true;
+  ev_out[0] = t->ev[pick][0];
+  ev_out[1] = t->ev[pick][1];
+  return kSchedCand[pick];
 }
 
 // ---------------------------------------------------------------------------
@@ -1483,13 +1493,18 @@ hipError_t launch_topk(do_dtype dt, SegTable& tab, int nseg, const PathArgs& a, 
   hipEvent_t ev[2] = {nullptr, nullptr};
   const int forced = g_opt_sched.load(std::memory_order_relaxed);
   const Sched sc = forced >= 0 ? kSchedCand[forced] : tuned_schedule(dt, tab, a, fast, s, ev);
-  if (ev[0] != nullptr) {
+  // a tuner trial binds its events to the dispatch (the kernel alone), unless
+  // the caller's timing events already are; then they go around the launch
+  ProfEv use = pe;
+  const bool around = ev[0] != nullptr && (pe.start != nullptr || pe.stop != nullptr);
+  if (ev[0] != nullptr && !around) use = ProfEv{ev[0], ev[1]};
+  if (around) {
     const hipError_t e = hipEventRecord(ev[0], s);
     if (e != hipSuccess) return e;
   }
   const hipError_t e =
-      dt == DO_F32 ? launch_ep<float>(tab, a, fast, sc, s, pe) : launch_ep<uint16_t>(tab, a, fast, sc, s, pe);
-  if (e != hipSuccess || ev[1] == nullptr) return e;
+      dt == DO_F32 ? launch_ep<float>(tab, a, fast, sc, s, use) : launch_ep<uint16_t>(tab, a, fast, sc, s, use);
+  if (e != hipSuccess || !around) return e;
   return hipEventRecord(ev[1], s);
 }
 

@@ -39,9 +39,9 @@ def _same_results(dl, scores, k, ref, label):
 
 
 def _schedules_and_grams_agree(dl, scores, k, ref, name):
-    """Both fixed unit schedules, the popcount Gram, and five calls with the
-    run-time choice (the schedule tuner measures both candidates on the first
-    calls of a shape and then keeps one) all reproduce `ref`."""
+    """Both fixed unit schedules, the popcount Gram, and eight calls with the
+    run-time choice (the schedule tuner measures each candidate three times on
+    the first calls of a shape and then keeps one) all reproduce `ref`."""
     try:
         for opt, val, label in ((dl.DO_OPT_SCHEDULE, 0, "XCD-partitioned schedule"),
                                 (dl.DO_OPT_SCHEDULE, 1, "contiguous schedule")):
@@ -53,7 +53,7 @@ def _schedules_and_grams_agree(dl, scores, k, ref, name):
         print(f"[case] {name}: popcount Gram", flush=True)
         _same_results(dl, scores, k, ref, f"{name} popcount Gram")
         dl.set_option(dl.DO_OPT_GRAM, 0)
-        for rep in range(5):
+        for rep in range(8):
             print(f"[case] {name}: tuned call {rep}", flush=True)
             _same_results(dl, scores, k, ref, f"{name} tuned call {rep}")
     finally:
