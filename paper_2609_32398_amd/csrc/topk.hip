@@ -41,6 +41,7 @@
 // and at the end (order-independent).
 #include <algorithm>
 #include <atomic>
+#include <chrono>
 #include <cstdio>
 #include <cstdlib>
 #include <mutex>
@@ -1256,8 +1257,11 @@ hipError_t launch_ep(const SegTable& tab, const PathArgs& a, bool fast, Sched sc
 // events around them; completed measurements are collected with
 // hipEventQuery, which never waits, and once every candidate has kTuneTrials
 // of them, the one with the fastest launch is used for all later launches of
-// that shape (it must beat the first candidate by 2 %).  The very first
-// launch of a shape is not measured (cold caches and TLB).  Launches under stream capture and
+// that shape (it must beat the first candidate by 2 %).  Measuring starts
+// kTuneDelayMs after the first launch of a shape: launches right after an idle
+// period run slower for some tens of milliseconds (7.3 ms falling to 5.6 ms
+// over the first six launches of workload 4), which would hide a 12 %
+// difference between the schedules.  Launches under stream capture and
 // launches below kTuneMinUnits use the first candidate (or the one already
 // chosen for the shape); a capture never touches the measurement events.
 // When every slot of the table holds a shape, a decided one is recycled.
@@ -1265,12 +1269,14 @@ constexpr Sched kSchedCand[2] = {Sched{4, true}, Sched{0, false}};  // XCD parti
 constexpr int kNumCand = 2;
 constexpr int64_t kTuneMinUnits = 1024;  // 512 Ki tokens
 constexpr int kTuneTrials = 3;           // measured launches per candidate
+constexpr double kTuneDelayMs = 100.0;   // no measurement before this long after a shape's first launch
 constexpr int kTuneSlots = 16;
 
 struct Tune {
   uint64_t key;
   int device;
   int calls;
+  std::chrono::steady_clock::time_point first;  // host time of the shape's first launch
   int chosen;                 // index into kSchedCand, or -1 while measuring
   float best[kNumCand];       // fastest completed launch per candidate (ms), < 0 if none yet
   int trials[kNumCand];       // completed measurements per candidate
@@ -1376,7 +1382,9 @@ Sched tuned_schedule(do_dtype dt, const SegTable& tab, const PathArgs& a, bool f
     decide(*t, bc);
     return kSchedCand[bc];
   }
-  if (t->calls++ == 0) return kSchedCand[0];
+  const auto now = std::chrono::steady_clock::now();
+  if (t->calls++ == 0) t->first = now;
+  if (std::chrono::duration<double, std::milli>(now - t->first).count() < kTuneDelayMs) return kSchedCand[0];
   // the candidate with the fewest measurements that has none in flight
   // (ties to the one measured least recently, so the candidates alternate)
   int pick = -1;

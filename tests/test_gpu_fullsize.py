@@ -10,6 +10,8 @@ library can choose and both Gram kinds are run at full size and must give
 bit-identical results; so must repeated calls while the schedule tuner
 measures its candidates.
 """
+import time
+
 import numpy as np
 import pytest
 import torch
@@ -40,8 +42,9 @@ def _same_results(dl, scores, k, ref, label):
 
 def _schedules_and_grams_agree(dl, scores, k, ref, name):
     """Both fixed unit schedules, the popcount Gram, and eight calls with the
-    run-time choice (the schedule tuner measures each candidate three times on
-    the first calls of a shape and then keeps one) all reproduce `ref`."""
+    run-time choice (from 100 ms after a shape's first launch the schedule
+    tuner measures each candidate three times, then keeps one) all reproduce
+    `ref`."""
     try:
         for opt, val, label in ((dl.DO_OPT_SCHEDULE, 0, "XCD-partitioned schedule"),
                                 (dl.DO_OPT_SCHEDULE, 1, "contiguous schedule")):
@@ -53,6 +56,7 @@ def _schedules_and_grams_agree(dl, scores, k, ref, name):
         print(f"[case] {name}: popcount Gram", flush=True)
         _same_results(dl, scores, k, ref, f"{name} popcount Gram")
         dl.set_option(dl.DO_OPT_GRAM, 0)
+        time.sleep(0.15)  # the tuner measures from 100 ms after a shape's first launch
         for rep in range(8):
             print(f"[case] {name}: tuned call {rep}", flush=True)
             _same_results(dl, scores, k, ref, f"{name} tuned call {rep}")

@@ -5,6 +5,8 @@ cleared with fill kernels, not memsets), so a captured do_fused replays to the
 same bits, distances and loss as an eager call.  Every replay is checked, with
 eager work and synchronisations between the replays.
 """
+import time
+
 import numpy as np
 import pytest
 import torch
@@ -134,8 +136,9 @@ def test_stream_reset_append_finalize_replays_from_a_graph(dl, syn, E, k):
 
 def test_capture_while_the_schedule_tuner_is_measuring(dl, syn):
     # 4,194,304 tokens = 8,192 work units: the run-time schedule choice
-    # applies.  The first eager call of the shape is unmeasured and the second
-    # leaves a measured trial pending, so the capture happens while the tuner
+    # applies.  The first eager call of the shape is unmeasured; the tuner
+    # measures only from 100 ms after it, so after a pause the second call
+    # leaves a measured trial pending and the capture happens while the tuner
     # is mid-way; a captured launch must not touch the measurement events and
     # must replay to the eager result, and eager calls after the capture
     # (which finish the measurement) must agree too.
@@ -144,6 +147,7 @@ def test_capture_while_the_schedule_tuner_is_measuring(dl, syn):
     xd = to_dev(syn.normal(909, N, E, 1))
     ref = dl.do_fused(xd, k, want_bits=True)
     torch.cuda.synchronize()
+    time.sleep(0.15)
     again = dl.do_fused(xd, k, want_bits=True)  # a measured trial
     bits = torch.zeros_like(ref[0])
     D = torch.zeros_like(ref[1])
