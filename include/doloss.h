@@ -26,9 +26,18 @@
  *   do_last_error() gives a message for the calling thread's last error.
  * - Layouts (all row-major, little-endian):
  *     scores  [L][N][E]  fp32 or bf16 (raw bf16 bit patterns)
- *     bits    [L][E][W]  uint64, W = ceil(N / 64); token t of expert e is bit
- *                        (t % 64) of word t / 64 (least significant bit first);
- *                        bits past N are zero
+ *     bits    [L][U][E][8]  uint64 signature words, U = ceil(N / 512) units of
+ *                        512 tokens (unit-major).  Word w (tokens 64w .. 64w +
+ *                        63) of expert e is element [w / 8][e][w % 8] of its
+ *                        layer; token t is bit (t % 64) of word t / 64 (least
+ *                        significant bit first); bits past N in word
+ *                        ceil(N/64) - 1 are zero.  A layer is E * Wp words,
+ *                        Wp = 8 * U ("padded words per expert"); the words
+ *                        past ceil(N/64) of the last unit are neither written
+ *                        nor read.  One unit of every expert is 64 * E
+ *                        contiguous bytes, which the Top-K kernel writes at
+ *                        once (Sec. 3.1.1 defines F_i as N bits per expert;
+ *                        the tiling is this library's).
  *     D       [L][E][E]  uint32, symmetric, zero diagonal
  *     out     [L]        do_loss_result
  * - Ranking rule for Top-K (the paper gives none; this is the library's reading):
@@ -78,7 +87,8 @@ typedef struct {
  * Steps 1-2 (Sec. 3.1.1, Eq. 1): Top-k of every token's scores and the packed
  * load signatures.
  *   scores  [L][N][E] device, dtype `dtype`
- *   bits    [L][E][ceil(N/64)] device, fully overwritten
+ *   bits    [L][U][E][8] device (signature layout above); the words of
+ *           tokens 0 .. N-1 are overwritten
  */
 do_status do_topk_signature(const void* scores, do_dtype dtype, int64_t N, int32_t E, int32_t k, int32_t L,
                             uint64_t* bits, hipStream_t stream);
@@ -87,8 +97,8 @@ do_status do_topk_signature(const void* scores, do_dtype dtype, int64_t N, int32
  * Step 3 (Sec. 3.1.3, Eq. 6 magnitude term; App. C.3 identity): the Hamming
  * distance matrix of existing signatures, computed as
  * D_ij = c_ii + c_jj - 2 c_ij with c_ij = popcount(F_i AND F_j).
- *   bits  [L][E][ceil(N/64)] device; bits past N must be zero (else the
- *         result is undefined)
+ *   bits  [L][U][E][8] device (signature layout); bits past N in the last
+ *         word must be zero (else the result is undefined)
  *   D     [L][E][E] device, fully overwritten
  */
 do_status do_pairwise_hamming(const uint64_t* bits, int64_t N, int32_t E, int32_t L, uint32_t* D,
@@ -112,7 +122,7 @@ do_status do_loss(const uint32_t* D, int32_t E, int32_t L, do_loss_result* out, 
  * accumulated in `D` itself, which is then turned into distances and reduced
  * to the loss.  Results are identical to do_topk_signature +
  * do_pairwise_hamming + do_loss.
- *   bits  [L][E][ceil(N/64)] device; may be NULL only for E <= 256 (wider E
+ *   bits  [L][U][E][8] device; may be NULL only for E <= 256 (wider E
  *         re-reads the stored signatures for the Gram: DO_ERR_INVALID_ARG)
  *   D     [L][E][E] device, fully overwritten
  *   out   [L] device
@@ -131,7 +141,7 @@ do_status do_fused(const void* scores, do_dtype dtype, int64_t N, int32_t E, int
  * data-parallel ranks, scale = 1/R gives the averaged magnitude of Eq. 8).
  *   p     [L][N][E] device, fp32 or bf16 routing probabilities (as given),
  *         aligned to two elements
- *   bits  [L][E][ceil(N/64)] device: the tokens' signatures (f_it = bit)
+ *   bits  [L][U][E][8] device: the tokens' signatures (f_it = bit)
  *   D     [L][E][E] device
  *   loss  [L] device doubles, overwritten
  *   grad  nullable, [L][N][E] device fp32 (8-byte aligned), overwritten
@@ -159,9 +169,12 @@ typedef struct {
  * diagonal of the co-occurrence counts, App. C.3), the Local-LBL balance loss
  * of Sec. 4.2 and the MaxVio imbalance of App. E for a placement of the
  * experts on ranks (L_r = sum of the loads of the experts on rank r).
- *   bits         [L][E][ld] device, ld = words per expert row (0 means
- *                ceil(N/64); a stream history uses do_stream_words_per_expert);
- *                bits past N must be zero
+ *   bits         device signatures in the signature layout, the layers
+ *                E * ld words apart; ld = padded words per expert, a
+ *                multiple of 8 of at least 8 * ceil(N/512) (0 means that
+ *                minimum; a stream history passes
+ *                do_stream_words_per_expert); bits past N in the last word
+ *                must be zero
  *   p            nullable, [L][N][E] device routing probabilities (fp32 or
  *                bf16, aligned to the element); NULL leaves lbl at 0
  *   expert_rank  nullable HOST array [E] of ranks in [0, R), read during the
@@ -188,7 +201,8 @@ do_status do_load_stats(const uint64_t* bits, int64_t N, int64_t ld, int32_t E, 
  */
 typedef struct do_stream_s do_stream;
 
-/* Allocates the history (E x ceil(capacity/64) words) and the counters on the
+/* Allocates the history (E x 8 * ceil(capacity/512) words, the signature
+ * layout of one layer) and the counters on the
  * current device and zeroes them (synchronously).  *out receives the handle,
  * or NULL on failure (DO_ERR_HIP when a device or host allocation fails). */
 do_status do_stream_create(int32_t E, int32_t k, int64_t capacity_tokens, do_stream** out);
@@ -222,11 +236,13 @@ do_status do_stream_reset(do_stream* h, hipStream_t stream);
  * current device is restored).  NULL is accepted. */
 do_status do_stream_destroy(do_stream* h);
 
-/* Device pointer to the history [E][do_stream_words_per_expert(h)].  Words
- * 0 .. ceil(do_stream_tokens(h) / 64) - 1 of every row hold the signatures of
- * the appended tokens, with zero bits past the last token; words after them
- * are zero until the first reset and unspecified after it (they may keep bits
- * of tokens appended before the reset). */
+/* Device pointer to the history: one layer in the signature layout with
+ * do_stream_words_per_expert(h) padded words per expert (E times that in
+ * total).  Words 0 .. ceil(do_stream_tokens(h) / 64) - 1 of every expert hold
+ * the signatures of the appended tokens, with zero bits past the last token;
+ * words after them are zero until the first reset and unspecified after it
+ * (they may keep bits of tokens appended before the reset).  A prefix of the
+ * history is itself a valid signature array for N = do_stream_tokens(h). */
 const uint64_t* do_stream_bits(const do_stream* h);
 int64_t do_stream_tokens(const do_stream* h);
 int64_t do_stream_words_per_expert(const do_stream* h);
@@ -253,8 +269,9 @@ do_status do_profile_next(hipEvent_t start, hipEvent_t stop);
  * process ends), which every call clears before use.
  *   scores         HOST array of `count` (1..64) device pointers, each
  *                  [n_tokens_each][E], read during the call
- *   hist           [E][ceil(count * n_tokens_each / 64)] device: the signatures
- *                  of the tokens in order (as do_stream_bits), overwritten
+ *   hist           [U][E][8] device, U = ceil(count * n_tokens_each / 512):
+ *                  the signatures of the tokens in order (signature layout,
+ *                  as do_stream_bits), overwritten
  *   D, out         as do_stream_finalize
  * Limits: E <= 256 (DO_ERR_INVALID_ARG otherwise), 1 <= k <= E,
  * n_tokens_each >= 1, count * n_tokens_each < 2^32 and the limits of

@@ -7,7 +7,8 @@ binding's functions raises.
 
 Functions keep the C names:
 
-* ``do_topk_signature(scores, k)``  -> bits  [L][E][ceil(N/64)] int64 (uint64 bit patterns)
+* ``do_topk_signature(scores, k)``  -> bits  [L][U][E][8] int64 (uint64 bit patterns), U = ceil(N/512):
+  word w of expert e is bits[l, w // 8, e, w % 8] (the library's unit-major signature layout)
 * ``do_pairwise_hamming(bits, N)``   -> D     [L][E][E] int32 (uint32 values)
 * ``do_loss(D)``                     -> out   [L][5] (sum, sumsq, loss, mean, var) as a dict list
 * ``do_fused(scores, k, want_bits)`` -> (bits or None, D, out)
@@ -159,8 +160,9 @@ def _scores_3d(scores: torch.Tensor, name: str = "scores"):
     return scores.shape[0], scores.shape[1], scores.shape[2]
 
 
-def _words(N: int) -> int:
-    return (N + 63) // 64
+def _units(N: int) -> int:
+    """512-token units of the signature layout."""
+    return (N + 511) // 512
 
 
 def set_option(option: int, value: int):
@@ -181,7 +183,8 @@ def loss_records(out: torch.Tensor) -> list[dict]:
 
 
 def alloc_bits(L: int, N: int, E: int, device) -> torch.Tensor:
-    return torch.empty((L, E, (N + 63) // 64), dtype=torch.int64, device=device)
+    """Signatures [L, U, E, 8], U = ceil(N/512) (see include/doloss.h)."""
+    return torch.empty((L, _units(N), E, 8), dtype=torch.int64, device=device)
 
 
 def alloc_D(L: int, E: int, device) -> torch.Tensor:
@@ -196,20 +199,20 @@ def do_topk_signature(scores: torch.Tensor, k: int, bits: torch.Tensor | None = 
     L, N, E = _scores_3d(scores)
     if bits is None:
         bits = alloc_bits(L, N, E, scores.device)
-    _want(bits, "bits", numel=L * E * _words(N), dtypes=_I64)
+    _want(bits, "bits", numel=L * E * 8 * _units(N), dtypes=_I64)
     _check(lib().do_topk_signature(scores.data_ptr(), _dtype_code(scores), N, E, k, L, bits.data_ptr(), _stream()),
            "do_topk_signature")
     return bits
 
 
 def do_pairwise_hamming(bits: torch.Tensor, N: int, D: torch.Tensor | None = None) -> torch.Tensor:
-    if not isinstance(bits, torch.Tensor) or bits.dim() not in (2, 3):
-        raise ValueError("bits must be a tensor of shape [E, W] or [L, E, W]")
-    if bits.dim() == 2:
+    if not isinstance(bits, torch.Tensor) or bits.dim() not in (3, 4) or bits.shape[-1] != 8:
+        raise ValueError("bits must be a tensor of shape [U, E, 8] or [L, U, E, 8]")
+    if bits.dim() == 3:
         bits = bits.unsqueeze(0)
-    L, E, W = bits.shape
-    if W != _words(N):
-        raise ValueError(f"bits has {W} words per expert, ceil(N/64) = {_words(N)} for N = {N}")
+    L, U, E = bits.shape[0], bits.shape[1], bits.shape[2]
+    if U != _units(N):
+        raise ValueError(f"bits has {U} units, ceil(N/512) = {_units(N)} for N = {N}")
     _want(bits, "bits", dtypes=_I64)
     if D is None:
         D = alloc_D(L, E, bits.device)
@@ -242,7 +245,7 @@ def do_fused(scores: torch.Tensor, k: int, want_bits: bool = False, bits: torch.
     if out is None:
         out = alloc_out(L, scores.device)
     if bits is not None:
-        _want(bits, "bits", numel=L * E * _words(N), dtypes=_I64)
+        _want(bits, "bits", numel=L * E * 8 * _units(N), dtypes=_I64)
     _want(D, "D", numel=L * E * E, dtypes=_I32)
     _want(out, "out", numel=L * LOSS_RESULT_BYTES, dtypes=_U8)
     _check(lib().do_fused(scores.data_ptr(), _dtype_code(scores), N, E, k, L,
@@ -255,7 +258,7 @@ def do_surrogate(p: torch.Tensor, k: int, bits: torch.Tensor, D: torch.Tensor, s
                  want_grad: bool = True, loss: torch.Tensor | None = None, grad: torch.Tensor | None = None):
     """Eq. (7) surrogate loss per layer (float64 [L]) and dloss/dp (float32 [L, N, E] or None)."""
     L, N, E = _scores_3d(p, "p")
-    _want(bits, "bits", numel=L * E * _words(N), dtypes=_I64)
+    _want(bits, "bits", numel=L * E * 8 * _units(N), dtypes=_I64)
     _want(D, "D", numel=L * E * E, dtypes=_I32)
     if loss is None:
         loss = torch.empty(L, dtype=torch.float64, device=p.device)
@@ -274,17 +277,19 @@ def do_load_stats(bits: torch.Tensor, N: int, k: int, p: torch.Tensor | None = N
                   R: int = 0, ld: int = 0, bits_ptr: int | None = None, E: int | None = None, L: int | None = None,
                   loads: torch.Tensor | None = None, out: torch.Tensor | None = None):
     """Per-expert loads (uint32 as int32 [L, E]) and per-layer statistics ([L, 32] bytes, see
-    load_stats_records) of signatures `bits` [L, E, ld or ceil(N/64)] (or a raw device pointer
-    `bits_ptr` with E and L given, e.g. a stream history).  p: routing probabilities [L, N, E] or
-    None; expert_rank: host sequence of E ranks in [0, R) or None (one expert per rank)."""
+    load_stats_records) of signatures `bits` [L, U, E, 8] with U >= ceil(N/512) (or a raw device
+    pointer `bits_ptr` with E, L and ld given, e.g. a stream history).  p: routing probabilities
+    [L, N, E] or None; expert_rank: host sequence of E ranks in [0, R) or None (one expert per rank)."""
     if bits_ptr is None:
-        if not isinstance(bits, torch.Tensor) or bits.dim() not in (2, 3):
-            raise ValueError("bits must be a tensor of shape [E, W] or [L, E, W]")
-        if bits.dim() == 2:
+        if not isinstance(bits, torch.Tensor) or bits.dim() not in (3, 4) or bits.shape[-1] != 8:
+            raise ValueError("bits must be a tensor of shape [U, E, 8] or [L, U, E, 8]")
+        if bits.dim() == 3:
             bits = bits.unsqueeze(0)
-        L, E = bits.shape[0], bits.shape[1]
-        if bits.shape[2] < max(ld, _words(N)):
-            raise ValueError(f"bits has {bits.shape[2]} words per expert, fewer than {max(ld, _words(N))}")
+        L, E = bits.shape[0], bits.shape[2]
+        if bits.shape[1] < _units(N):
+            raise ValueError(f"bits has {bits.shape[1]} units, fewer than ceil(N/512) = {_units(N)}")
+        if ld == 0:
+            ld = 8 * bits.shape[1]  # the tensor's layer stride
         _want(bits, "bits", dtypes=_I64)
         ptr = bits.data_ptr()
         dev = bits.device
@@ -337,7 +342,7 @@ def do_global_batch_noalloc(score_list, k: int, hist: torch.Tensor | None = None
                             out: torch.Tensor | None = None):
     """do_global_batch_noalloc: the history, distances and loss of one global batch of
     micro-batches (each [n, E] on the device) in one call that allocates nothing in the
-    library.  Returns (hist int64 [E, ceil(count n / 64)], D int32 [E, E], out [1, 40])."""
+    library.  Returns (hist int64 [U, E, 8] with U = ceil(count n / 512), D int32 [E, E], out [1, 40])."""
     if not 1 <= len(score_list) <= 64:
         raise ValueError("do_global_batch_noalloc takes 1 to 64 micro-batches")
     first = score_list[0]
@@ -348,14 +353,14 @@ def do_global_batch_noalloc(score_list, k: int, hist: torch.Tensor | None = None
         if not isinstance(t, torch.Tensor) or t.shape != first.shape or t.dtype != first.dtype:
             raise ValueError(f"scores[{i}] differs in shape or dtype from scores[0]")
         _want(t, f"scores[{i}]", dtypes=_SCORE_DTYPES)
-    W = _words(len(score_list) * n)
+    U = _units(len(score_list) * n)
     if hist is None:
-        hist = torch.empty((E, W), dtype=torch.int64, device=first.device)
+        hist = torch.empty((U, E, 8), dtype=torch.int64, device=first.device)
     if D is None:
         D = torch.empty((E, E), dtype=torch.int32, device=first.device)
     if out is None:
         out = alloc_out(1, first.device)
-    _want(hist, "hist", numel=E * W, dtypes=_I64)
+    _want(hist, "hist", numel=E * 8 * U, dtypes=_I64)
     _want(D, "D", numel=E * E, dtypes=_I32)
     _want(out, "out", numel=LOSS_RESULT_BYTES, dtypes=_U8)
     ptrs = (ctypes.c_void_p * len(score_list))(*[t.data_ptr() for t in score_list])
@@ -503,9 +508,10 @@ class DoStream:
         return int(lib().do_stream_bits(self.h) or 0)
 
     def history(self) -> torch.Tensor:
-        """Copy of the signature history [E][words_per_expert] (int64 words)."""
+        """Copy of the signature history [words_per_expert / 8, E, 8] (int64 words, signature layout)."""
         W = self.words_per_expert
-        out = torch.empty((self.E, W), dtype=torch.int64, device=torch.device("cuda", torch.cuda.current_device()))
+        out = torch.empty((W // 8, self.E, 8), dtype=torch.int64,
+                          device=torch.device("cuda", torch.cuda.current_device()))
         _check(_hip_copy_d2d(out.data_ptr(), self.bits_ptr(), self.E * W * 8), "history copy")
         return out
 

@@ -105,8 +105,7 @@ do_status run_layers(const void* scores, do_dtype dt, int64_t N, int32_t E, int3
   a.E = E;
   a.k = k;
   a.bits = bits;
-  a.bits_layer_words = (int64_t)E * W;
-  a.W = W;
+  a.bits_layer_words = (int64_t)E * dol::sig_words(W);
   a.or_partial = 0;
   a.cacc = cacc;
   a.cacc_layer_elems = (int64_t)E * E;
@@ -139,9 +138,9 @@ struct do_stream_s {
   int32_t E;
   int32_t k;
   int64_t capacity;
-  int64_t W;
+  int64_t W;        // signature words per expert: whole units (a multiple of 8)
   int64_t tokens;
-  u64* hist;        // [E][W], at the start of one allocation
+  u64* hist;        // E * W words in the signature layout (sig_off), at the start of one allocation
   uint32_t* cacc;   // kStreamCopies x [E][E] counters, after the history
   uint32_t* snap;   // [E][E]: the totals of the last finalize
   u64* fin;         // 3 words: the finalize's two sums and its ticket
@@ -203,7 +202,8 @@ DOLOSS_API do_status do_pairwise_hamming(const uint64_t* bits, int64_t N, int32_
   if (E <= dol::kFastMaxE && dol::gram_mfma_enabled())
     DO_TRY(hip_status(dol::launch_gram_mfma(reinterpret_cast<const u64*>(bits), W, E, L, D, stream), "gram"));
   else
-    DO_TRY(hip_status(dol::launch_gram_bits(reinterpret_cast<const u64*>(bits), W, W, E, L, D, stream), "gram"));
+    DO_TRY(hip_status(
+        dol::launch_gram_bits(reinterpret_cast<const u64*>(bits), W, dol::sig_words(W), E, L, D, stream), "gram"));
   return hip_status(dol::launch_finalize(D, D, nullptr, E, L, stream), "finalize");
 }
 
@@ -230,9 +230,9 @@ DOLOSS_API do_status do_fused(const void* scores, do_dtype dtype, int64_t N, int
     DO_TRY(run_layers(scores, dtype, N, E, k, L, reinterpret_cast<u64*>(bits), D, stream));
   } else {
     DO_TRY(run_layers(scores, dtype, N, E, k, L, reinterpret_cast<u64*>(bits), nullptr, stream));
+    const int64_t W = (N + 63) / 64;
     DO_TRY(hip_status(
-        dol::launch_gram_bits(reinterpret_cast<const u64*>(bits), (N + 63) / 64, (N + 63) / 64, E, L, D, stream),
-        "gram"));
+        dol::launch_gram_bits(reinterpret_cast<const u64*>(bits), W, dol::sig_words(W), E, L, D, stream), "gram"));
   }
   return hip_status(dol::launch_finalize(D, D, out, E, L, stream), "finalize");
 }
@@ -275,8 +275,9 @@ DOLOSS_API do_status do_load_stats(const uint64_t* bits, int64_t N, int64_t ld, 
   DO_TRY(check_shape(N, E, L));
   DO_TRY(check_k(k, E));
   const int64_t W = (N + 63) / 64;
-  if (ld == 0) ld = W;
-  if (ld < W) return fail(DO_ERR_INVALID_ARG, "ld must be 0 or at least ceil(N/64)");
+  if (ld == 0) ld = dol::sig_words(W);
+  if (ld < dol::sig_words(W) || ld % 8 != 0)
+    return fail(DO_ERR_INVALID_ARG, "ld must be 0, or a multiple of 8 of at least 8 * ceil(N/512)");
   if (bits == nullptr || !aligned(bits, 8)) return fail(DO_ERR_INVALID_ARG, "bits is NULL or not 8-byte aligned");
   if (loads == nullptr || !aligned(loads, 4)) return fail(DO_ERR_INVALID_ARG, "loads is NULL or not 4-byte aligned");
   if (out == nullptr || !aligned(out, 8)) return fail(DO_ERR_INVALID_ARG, "out is NULL or not 8-byte aligned");
@@ -375,7 +376,7 @@ DOLOSS_API do_status do_stream_create(int32_t E, int32_t k, int64_t capacity_tok
   h->E = E;
   h->k = k;
   h->capacity = capacity_tokens;
-  h->W = (capacity_tokens + 63) / 64;
+  h->W = dol::sig_words((capacity_tokens + 63) / 64);  // whole units
   h->tokens = 0;
   // one allocation: the history, the counter copies, the snapshot, the finalize words
   const int64_t mat_words = ((int64_t)E * E + 1) / 2;  // one E x E uint32 matrix, in u64 words
@@ -416,7 +417,7 @@ do_status check_handle(const do_stream* h) {
 hipError_t clear_history_words(do_stream* h, int64_t w0, int64_t w1, hipStream_t s) {
   if (w1 <= w0) return hipSuccess;
   if (w0 == 0 && w1 == h->W) return dol::launch_fill_u64(h->hist, (int64_t)h->E * h->W, s);
-  return dol::launch_fill_rows(h->hist, h->W, h->E, w0, w1 - w0, s);
+  return dol::launch_fill_sig_words(h->hist, h->E, w0, w1 - w0, s);
 }
 
 do_status stream_append(do_stream* h, const void* const* scores, do_dtype dtype, int64_t n, int32_t count,
@@ -450,7 +451,6 @@ do_status stream_append(do_stream* h, const void* const* scores, do_dtype dtype,
   a.k = h->k;
   a.bits = h->hist;
   a.bits_layer_words = (int64_t)h->E * h->W;
-  a.W = h->W;
   a.or_partial = 1;
   const bool gram = h->E <= dol::kFastMaxE;  // wider E: Gram of the whole history at finalize
   a.cacc = gram ? h->cacc : nullptr;
@@ -614,18 +614,17 @@ DOLOSS_API do_status do_global_batch_noalloc(const void* const* scores, do_dtype
   DO_TRY(scratch_on_device(&sp));
   uint32_t* cacc = reinterpret_cast<uint32_t*>(sp);
   u64* fin = sp + kNoAllocCountWords;
-  const int64_t W = (N + 63) / 64;
+  const int64_t Wp = dol::sig_words((N + 63) / 64);
   // every word the appends OR into starts at zero, and so do the counts and
   // the finalize's sums (fill kernels: no memset nodes under graph capture)
-  DO_TRY(hip_status(dol::launch_fill_u64(reinterpret_cast<u64*>(hist), (int64_t)E * W, stream), "fill history"));
+  DO_TRY(hip_status(dol::launch_fill_u64(reinterpret_cast<u64*>(hist), (int64_t)E * Wp, stream), "fill history"));
   DO_TRY(hip_status(dol::launch_fill_u64(sp, ((int64_t)E * E + 1) / 2, stream), "fill counters"));
   DO_TRY(hip_status(dol::launch_fill_u64(fin, 3, stream), "fill finalize words"));
   dol::PathArgs a{};
   a.E = E;
   a.k = k;
   a.bits = reinterpret_cast<u64*>(hist);
-  a.bits_layer_words = (int64_t)E * W;
-  a.W = W;
+  a.bits_layer_words = (int64_t)E * Wp;
   a.or_partial = 1;
   a.cacc = cacc;
   a.cacc_layer_elems = (int64_t)E * E;

@@ -40,12 +40,22 @@ struct SegTable {
 };
 
 // Where one launch writes its results.
+// Signature layout.  A layer of N tokens is U = ceil(N/512) units of 512
+// tokens, and unit u holds the 8 words of every expert, expert after expert
+// (word s of the unit: tokens 512u + 64s .. 512u + 64s + 63, bit b = token
+// 512u + 64s + b).  Word w of expert e sits at sig_off(w, e, E) words from
+// the layer's start, and a layer takes E * sig_words(W) words, W = ceil(N/64).
+// The Top-K kernel writes a unit's signatures as one contiguous block.
+__host__ __device__ __forceinline__ int64_t sig_words(int64_t W) { return (W + 7) & ~int64_t(7); }
+__host__ __device__ __forceinline__ int64_t sig_off(int64_t w, int64_t e, int64_t E) {
+  return ((w >> 3) * E + e) * 8 + (w & 7);
+}
+
 struct PathArgs {
   int32_t E;
   int32_t k;
-  u64* bits;                // nullable: signatures [layer][E][W]
+  u64* bits;                // nullable: signatures, the layers E * sig_words(W) words apart (sig_off)
   int64_t bits_layer_words; // words per layer of `bits`
-  int64_t W;                // words per expert row of `bits`
   int32_t or_partial;       // words shared with other segments are OR-ed (history), else stored
   int32_t ncopies;          // copies of the accumulators (0 or 1: one); block b adds into copy b % ncopies
   uint32_t* cacc;           // nullable: co-occurrence accumulators [layer][E][E], upper triangle
@@ -56,7 +66,7 @@ struct PathArgs {
 // Arguments of the surrogate-loss kernel.
 struct SurrogateArgs {
   const void* p;       // [L][N][E] routing probabilities (fp32 or bf16)
-  const u64* bits;     // [L][E][W] signatures
+  const u64* bits;     // signatures (layout: sig_off), W = ceil(N/64) words per expert
   const uint32_t* D;   // [L][E][E] distances G
   double* loss;        // [L], accumulated into (zeroed by the caller)
   float* grad;         // nullable [L][N][E]
@@ -75,8 +85,8 @@ DevInfo device_info();
 
 hipError_t launch_fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s);
 hipError_t launch_fill_u64(u64* p, int64_t n, hipStream_t s);
-// Zeroes words [w0, w0 + nw) of `rows` rows that are ld words apart.
-hipError_t launch_fill_rows(u64* p, int64_t ld, int32_t rows, int64_t w0, int64_t nw, hipStream_t s);
+// Zeroes signature words [w0, w0 + nw) of all E experts of one layer at p.
+hipError_t launch_fill_sig_words(u64* p, int32_t E, int64_t w0, int64_t nw, hipStream_t s);
 
 // A caller's timing events for one kernel dispatch (either may be null):
 // bound to the dispatch itself, so their interval is that kernel's run.
@@ -91,11 +101,12 @@ hipError_t launch_topk(do_dtype dt, SegTable& tab, int nseg, const PathArgs& a, 
                        const ProfEv& pe = ProfEv{});
 
 // Co-occurrence counts of existing signatures: cacc[l][i][j] += popcount(F_i & F_j), i <= j,
-// over the first W words of rows that are ld words apart (layers E * ld words apart).
+// over words [0, W) of each expert; ld = words per expert of a layer (a
+// multiple of 8), layers E * ld words apart (signature layout: sig_off).
 hipError_t launch_gram_bits(const u64* bits, int64_t W, int64_t ld, int32_t E, int32_t L, uint32_t* cacc,
                             hipStream_t s);
 // The same Gram on fp4 MFMA tiles (E <= 256): counts added into cacc [L][E][E]
-// (upper triangle, zeroed by the caller).
+// (upper triangle, zeroed by the caller); layers E * sig_words(W) words apart.
 hipError_t launch_gram_mfma(const u64* bits, int64_t W, int32_t E, int32_t L, uint32_t* cacc, hipStream_t s);
 // False when do_set_option selects the popcount Gram (a comparison switch).
 bool gram_mfma_enabled();
@@ -117,8 +128,9 @@ struct RankMap {
   int32_t given;
 };
 
-// Load statistics: loads[l][e] = popcount of signature row e of layer l
-// (ld words per row, W = ceil(N/64) of them read); with p, the Local-LBL sum
+// Load statistics: loads[l][e] = popcount of the signature of expert e of
+// layer l (words [0, ceil(N/64)); ld = words per expert of a layer, a
+// multiple of 8, layers E * ld words apart); with p, the Local-LBL sum
 // accumulated into out[l].lbl (zeroed by the caller) and scaled in the
 // finalize, which also writes total / max / min / MaxVio.
 hipError_t launch_load_stats(const u64* bits, int64_t N, int64_t ld, int32_t E, int32_t k, int32_t L, const void* p,

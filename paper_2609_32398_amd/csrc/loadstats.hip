@@ -1,15 +1,16 @@
 // Load statistics of signatures: per-expert loads (App. C.3), the Local-LBL
 // balance loss (Sec. 4.2) and the MaxVio imbalance (App. E).
 //
-//   n_i     = popcount of signature row i (the tokens routed to expert i)
+//   n_i     = popcount of the signature of expert i (the tokens routed to it)
 //   lbl     = sum_i f_i P_i,  f_i = n_i / (N k),  P_i = (1/N) sum_t p_it
 //           = (1 / (N^2 k)) sum_i n_i sum_t p_it
 //   maxvio  = max_r |L_r / tau - 1|,  L_r = sum of n_i over the experts on
 //             rank r,  tau = mean of the L_r
 //
-// Three launches: k_row_loads (one block per signature row, a streaming
-// popcount), k_lbl_sums (column sums of p weighted by the loads, read once;
-// only when p is given) and k_load_finalize (one block per layer).
+// Four launches: a fill of the loads, k_unit_loads (a streaming popcount of
+// the signatures, unit by unit), k_lbl_sums (column sums of p weighted by the
+// loads, read once; only when p is given) and k_load_finalize (one block per
+// layer).
 #include <algorithm>
 
 #include "common.h"
@@ -34,22 +35,40 @@ __device__ __forceinline__ V block_sum(V v, V* red) {
   return t;  // valid in thread 0
 }
 
-// blockIdx.x = expert, blockIdx.y = layer.  Reads the W = ceil(N/64) words of
-// the row (bits past N are zero by contract).
-__global__ __launch_bounds__(kLsThreads) void k_row_loads(const u64* bits, int64_t W, int64_t ld, int32_t E,
-                                                          uint32_t* loads) {
-  __shared__ uint32_t red[kLsThreads / kWave];
-  const int e = blockIdx.x, l = blockIdx.y;
-  const u64* row = bits + ((int64_t)l * E + e) * ld;
-  uint32_t c = 0;
-  int64_t w = threadIdx.x;
-  for (; w + 3 * kLsThreads < W; w += 4 * kLsThreads) {  // four loads in flight per thread
-    const u64 a = row[w], b = row[w + kLsThreads], d = row[w + 2 * kLsThreads], f = row[w + 3 * kLsThreads];
-    c += (uint32_t)(__popcll(a) + __popcll(b) + __popcll(d) + __popcll(f));
+// grid = (blocks per layer, layers).  Block b takes a contiguous range of the
+// layer's units (signature layout: a unit is the 8 words of every expert,
+// E * 8 contiguous words; words at or past W are not counted).  Thread t
+// reads words f = t + 256 i of every unit, expert f / 8, so its experts are
+// fixed: t / 8 + 32 i, i < NE.  The eight lanes of an expert then sum their
+// counts, and one of them adds the sum into loads (zeroed by the caller).
+template <int NE>
+__global__ __launch_bounds__(kLsThreads) void k_unit_loads(const u64* bits, int64_t W, int64_t ld, int32_t E,
+                                                           uint32_t* loads) {
+  static_assert(kLsThreads == 256, "experts t / 8 + 32 i");
+  const int l = blockIdx.y, t = threadIdx.x, s = t & 7;
+  const int64_t U = (W + 7) >> 3;
+  const int64_t u0 = (int64_t)blockIdx.x * U / gridDim.x, u1 = (int64_t)(blockIdx.x + 1) * U / gridDim.x;
+  const u64* lb = bits + (int64_t)l * E * ld;
+  uint32_t c[NE];
+#pragma unroll
+  for (int i = 0; i < NE; ++i) c[i] = 0u;
+  for (int64_t u = u0; u < u1; ++u) {
+    const u64* ub = lb + u * E * 8;
+    const bool wv = 8 * u + s < W;
+#pragma unroll
+    for (int i = 0; i < NE; ++i) {
+      const int f = t + kLsThreads * i;
+      if (wv && f < 8 * E) c[i] += (uint32_t)__popcll(__builtin_nontemporal_load(ub + f));
+    }
   }
-  for (; w < W; w += kLsThreads) c += (uint32_t)__popcll(row[w]);
-  const uint32_t t = block_sum<uint32_t>(c, red);
-  if (threadIdx.x == 0) loads[(int64_t)l * E + e] = t;
+#pragma unroll
+  for (int i = 0; i < NE; ++i) {
+    c[i] += (uint32_t)__shfl_xor((int)c[i], 1);
+    c[i] += (uint32_t)__shfl_xor((int)c[i], 2);
+    c[i] += (uint32_t)__shfl_xor((int)c[i], 4);
+    const int e = (t >> 3) + 32 * i;
+    if (s == 0 && e < E && c[i] != 0u) atomicAdd(&loads[(int64_t)l * E + e], c[i]);
+  }
 }
 
 template <typename T>
@@ -183,8 +202,28 @@ hipError_t launch_load_stats(const u64* bits, int64_t N, int64_t ld, int32_t E, 
   const int64_t W = (N + 63) / 64;
   hipError_t e = launch_fill_u64(reinterpret_cast<u64*>(out), (int64_t)L * (sizeof(do_load_stats_result) / 8), s);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_row_loads, dim3((unsigned)E, (unsigned)L), dim3(kLsThreads), 0, s, bits, W, ld, E, loads);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if ((e = launch_fill_u32(loads, (int64_t)L * E, 0u, s)) != hipSuccess) return e;
+  {
+    // about four blocks per CU in total, each over a contiguous range of units
+    const DevInfo di = device_info();
+    const int64_t U = (W + 7) / 8;
+    const int64_t per_layer = std::max<int64_t>(1, std::min<int64_t>(U, ((int64_t)di.cu_count * 4 + L - 1) / L));
+    const dim3 grid((unsigned)per_layer, (unsigned)L);
+    const int ne = (E + 31) / 32;  // counters per thread
+    if (ne <= 1)
+      hipLaunchKernelGGL(k_unit_loads<1>, grid, dim3(kLsThreads), 0, s, bits, W, ld, E, loads);
+    else if (ne <= 2)
+      hipLaunchKernelGGL(k_unit_loads<2>, grid, dim3(kLsThreads), 0, s, bits, W, ld, E, loads);
+    else if (ne <= 4)
+      hipLaunchKernelGGL(k_unit_loads<4>, grid, dim3(kLsThreads), 0, s, bits, W, ld, E, loads);
+    else if (ne <= 8)
+      hipLaunchKernelGGL(k_unit_loads<8>, grid, dim3(kLsThreads), 0, s, bits, W, ld, E, loads);
+    else if (ne <= 16)
+      hipLaunchKernelGGL(k_unit_loads<16>, grid, dim3(kLsThreads), 0, s, bits, W, ld, E, loads);
+    else
+      hipLaunchKernelGGL(k_unit_loads<32>, grid, dim3(kLsThreads), 0, s, bits, W, ld, E, loads);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
   if (p != nullptr) {
     // about 8 blocks per CU in total, each over a contiguous slice of rows
     const DevInfo di = device_info();

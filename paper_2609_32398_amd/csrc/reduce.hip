@@ -46,16 +46,19 @@ __global__ void k_fill_u64(u64* p, int64_t n) {
   }
 }
 
-// Zeroes words [w0, w0 + nw) of `rows` rows that are ld words apart.
-__global__ void k_fill_rows(u64* p, int64_t ld, int rows, int64_t w0, int64_t nw) {
-  const int64_t total = (int64_t)rows * nw;
+// Zeroes signature words [w0, w0 + nw) of all E experts of one layer
+// (unit-major layout, sig_off).
+__global__ void k_fill_sig_words(u64* p, int E, int64_t w0, int64_t nw) {
+  const int64_t total = (int64_t)E * nw;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (int64_t)gridDim.x * blockDim.x)
-    p[(i / nw) * ld + w0 + i % nw] = 0ull;
+    p[sig_off(w0 + i / E, i % E, E)] = 0ull;
 }
 
 // grid = (word-chunk blocks, micro-tile slices, layers).  Each thread owns up
 // to kGramMtq 4x4 micro-tiles of the upper triangle and accumulates
-// popcount(F_i & F_j) over the word chunks of its block in registers.
+// popcount(F_i & F_j) over the word chunks of its block in registers.  A
+// chunk is one unit of the signature layout (8 words of every expert, E * 64
+// contiguous bytes); layers are E * ld words apart.
 __global__ __launch_bounds__(kGramThreads) void k_gram_bits(const u64* __restrict__ bits, int64_t W, int64_t ld,
                                                             int E, uint32_t* __restrict__ cacc) {
   extern __shared__ __align__(16) u64 tile[];  // [kGramSlots][E4]
@@ -101,7 +104,7 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bits(const u64* __restric
       for (int b = 0; b < kB; ++b) {
         const int f = f0 + b * kGramThreads, e = f / kGramSlots, s = f % kGramSlots;
         const bool in = f < total && e < E && w0 + s < W;
-        v[b] = lb[in ? (int64_t)e * ld + w0 + s : 0];
+        v[b] = lb[in ? sig_off(w0 + s, e, E) : 0];
         v[b] = in ? v[b] : 0ull;
       }
 #pragma unroll
@@ -546,11 +549,11 @@ hipError_t launch_finalize_stream(uint32_t* copies, int32_t ncopies, int64_t cop
   return hipGetLastError();
 }
 
-hipError_t launch_fill_rows(u64* p, int64_t ld, int32_t rows, int64_t w0, int64_t nw, hipStream_t s) {
-  if (rows <= 0 || nw <= 0) return hipSuccess;
-  const int64_t total = (int64_t)rows * nw;
+hipError_t launch_fill_sig_words(u64* p, int32_t E, int64_t w0, int64_t nw, hipStream_t s) {
+  if (E <= 0 || nw <= 0) return hipSuccess;
+  const int64_t total = (int64_t)E * nw;
   const int64_t blocks = std::min<int64_t>((total + 255) / 256, 4096);
-  hipLaunchKernelGGL(k_fill_rows, dim3((unsigned)blocks), dim3(256), 0, s, p, ld, rows, w0, nw);
+  hipLaunchKernelGGL(k_fill_sig_words, dim3((unsigned)blocks), dim3(256), 0, s, p, E, w0, nw);
   return hipGetLastError();
 }
 

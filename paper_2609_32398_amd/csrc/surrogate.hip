@@ -85,8 +85,7 @@ template <typename T, bool FULL, bool GRAD>
 __device__ __forceinline__ void surrogate_item(const SurrogateArgs& a, const uint32_t* gt, WaveLists& wl, int E,
                                                int ng, int iw, int r, int layer, int64_t w, int32_t R0, int32_t R1,
                                                double& lacc, int lane) {
-  const int64_t W = a.W;
-  const u64* bl = a.bits + (int64_t)layer * E * W;
+  const u64* bl = a.bits + (int64_t)layer * E * sig_words(a.W);
   const int il0 = 2 * lane;
   const bool v0 = FULL || il0 < iw, v1 = FULL || il0 + 1 < iw;
   const bool even = FULL || (E & 1) == 0;
@@ -94,7 +93,7 @@ __device__ __forceinline__ void surrogate_item(const SurrogateArgs& a, const uin
   // words of experts g*64 + lane
   u64 wg[4];
 #pragma unroll
-  for (int g = 0; g < 4; ++g) wg[g] = (g < ng && g * 64 + lane < E) ? bl[(int64_t)(g * 64 + lane) * W + w] : 0ull;
+  for (int g = 0; g < 4; ++g) wg[g] = (g < ng && g * 64 + lane < E) ? bl[sig_off(w, g * 64 + lane, E)] : 0ull;
   // token lists: expert g*64 + lane appends its row offset to the list of
   // every token whose bit is set in its word (order within a list is
   // irrelevant: summed)

@@ -891,9 +891,12 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
   // stores when the unit starts on an even word, else word by word.
   // The stores of plain units (8 words, even first word, no word shared with
   // a neighbouring segment) are held in registers for up to SB::kUnits
-  // consecutive units of one layer and issued together, so each expert row
-  // receives 64 * SB::kUnits contiguous bytes at once (fewer read/write
-  // turnarounds in HBM than one 64-byte piece per unit).  Only for E <= 256.
+  // consecutive units of one layer and issued together.  In the unit-major
+  // signature layout a unit that starts on a multiple of 8 words is one
+  // contiguous block of E * 64 bytes, so a block's batch writes up to
+  // SB::kUnits * E * 64 contiguous bytes (with expert-major rows, 64-byte
+  // pieces 256 rows apart cost up to 1 ms more per 1 GiB on some buffer
+  // placements; contiguous blocks 0.4 ms).  Only for E <= 256.
   // Whole-vector stores carry the non-temporal hint: the signatures are not
   // read again by this kernel.
   auto batch_flush = [&]() __attribute__((always_inline)) {
@@ -903,10 +906,10 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
     for (int i = 0; i < SB::kItems; ++i) {
       const int item = e_lo * 4 + lane + i * kWave;
       if (item < e_hi * 4) {
-        u64* dst = sb_lb + (int64_t)(item >> 2) * a.W + sb_w0 + (item & 3) * 2;
+        u64* dst = sb_lb + sig_off(sb_w0 + (item & 3) * 2, item >> 2, E);
 #pragma unroll
-        for (int j = 0; j < SB::kUnits; ++j)
-          if (j < sb_n) __builtin_nontemporal_store(sreg[j][i], reinterpret_cast<v2u64*>(dst + 8 * j));
+        for (int j = 0; j < SB::kUnits; ++j)  // unit j of the batch: 8 words further for every expert
+          if (j < sb_n) __builtin_nontemporal_store(sreg[j][i], reinterpret_cast<v2u64*>(dst + (int64_t)E * 8 * j));
       }
     }
     sb_n = 0;
@@ -942,23 +945,36 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
     batch_flush();
     auto plain = [&](int s_) { return !((s_ == 0 && pend.shared_lo) || s_ == pend.shared_hi); };
     auto put = [&](int e_, int s_, u64 word) {
-      u64* dst = pend.lb + (int64_t)e_ * a.W + pend.w0 + s_;
+      u64* dst = pend.lb + sig_off(pend.w0 + s_, e_, E);
       if (plain(s_))
         *dst = word;
       else if (word)
         atomicOr(dst, word);
     };
+    // without or_partial a segment is a whole layer that starts on a unit, so
+    // the words of its last unit past the segment are the layer's padding:
+    // they are written as zeros (the output is then fully determined)
+    const bool pad = a.or_partial == 0;
     if ((pend.w0 & 1) == 0) {
       for (int item = e_lo * 4 + lane; item < e_hi * 4; item += kWave) {
         const int e = item >> 2, s0 = (item & 3) * 2;
-        if (s0 >= pend.cnt) continue;
+        if (s0 >= pend.cnt) {
+          if (pad)
+            __builtin_nontemporal_store(v2u64{0ull, 0ull},
+                                        reinterpret_cast<v2u64*>(pend.lb + sig_off(pend.w0 + s0, e, E)));
+          continue;
+        }
         const u64 wa = pbt[s0 * EPW + (e ^ bt_swz(s0))];
         const u64 wb = pbt[(s0 + 1) * EPW + (e ^ bt_swz(s0 + 1))];
         if (s0 + 1 < pend.cnt && plain(s0) && plain(s0 + 1)) {
-          __builtin_nontemporal_store(v2u64{wa, wb}, reinterpret_cast<v2u64*>(pend.lb + (int64_t)e * a.W + pend.w0 + s0));
+          // an even word and the next lie in one unit: 16 contiguous bytes
+          __builtin_nontemporal_store(v2u64{wa, wb}, reinterpret_cast<v2u64*>(pend.lb + sig_off(pend.w0 + s0, e, E)));
         } else {
           put(e, s0, wa);
-          if (s0 + 1 < pend.cnt) put(e, s0 + 1, wb);
+          if (s0 + 1 < pend.cnt)
+            put(e, s0 + 1, wb);
+          else if (pad)
+            put(e, s0 + 1, 0ull);
         }
       }
     } else {
@@ -1435,7 +1451,7 @@ __global__ __launch_bounds__(kFusedThreads) void k_gram_mfma(const u64* bits, in
   const int64_t nch = (W + kFusedWaves - 1) / kFusedWaves;
   const int64_t c0 = part * nch / bpl, c1 = (part + 1) * nch / bpl;
   if (c0 >= c1) return;
-  const u64* lb = bits + (int64_t)l * E * W;
+  const u64* lb = bits + (int64_t)l * E * sig_words(W);
   const WaveTiles wt = wave_tiles(GS::T, wave);
   Acc acc[kGP];
 #pragma unroll
@@ -1443,8 +1459,8 @@ __global__ __launch_bounds__(kFusedThreads) void k_gram_mfma(const u64* bits, in
 #pragma unroll
     for (int r = 0; r < Mfma<GS::TS>::kRegs; ++r) acc[p][r] = 0.0f;
   // thread tid holds words (e, s) = (idx / 8, idx % 8) for idx = tid + q * 512
-  // of each chunk: eight threads read an expert's 64 contiguous bytes; chunks
-  // at or past c1 read as zero
+  // of each chunk: a chunk is one unit of the signature layout, E * 64
+  // contiguous bytes; chunks at or past c1 read as zero
   u64 r[kGramGroup][kPer];
   auto load = [&](int64_t g0) {
 #pragma unroll
@@ -1454,7 +1470,7 @@ __global__ __launch_bounds__(kFusedThreads) void k_gram_mfma(const u64* bits, in
         const int idx = tid + q * kFusedThreads, e = idx >> 3;
         const int64_t w = (g0 + g) * kFusedWaves + (idx & 7);
         r[g][q] = (idx < kTileWords && g0 + g < c1 && e < E && w < W)
-                      ? __builtin_nontemporal_load(lb + (int64_t)e * W + w)
+                      ? __builtin_nontemporal_load(lb + sig_off(w, e, E))
                       : 0ull;
       }
   };

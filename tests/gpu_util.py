@@ -12,9 +12,27 @@ def to_dev(scores: np.ndarray) -> torch.Tensor:
     raise TypeError(scores.dtype)
 
 
-def bits_np(bits: torch.Tensor) -> np.ndarray:
-    """int64 device tensor of uint64 words -> numpy uint64."""
-    return bits.cpu().numpy().view(np.uint64)
+def bits_np(bits: torch.Tensor, N: int | None = None) -> np.ndarray:
+    """Signatures in the library's unit-major layout ([..., U, E, 8] int64 on the device)
+    -> expert-major numpy uint64 [..., E, W]: W = ceil(N/64) words when N is given (the
+    words past it in the last unit are never written), else all 8 U."""
+    a = bits.cpu().numpy().view(np.uint64)
+    assert a.shape[-1] == 8, a.shape
+    a = np.swapaxes(a, -3, -2)  # [..., E, U, 8]
+    a = a.reshape(a.shape[:-2] + (a.shape[-2] * 8,))
+    return np.ascontiguousarray(a if N is None else a[..., : (N + 63) // 64])
+
+
+def units_dev(words: np.ndarray) -> torch.Tensor:
+    """Expert-major signature words [..., E, W] (numpy uint64, e.g. the oracle's pack) ->
+    the library's unit-major layout [..., U, E, 8] on the device, zero words past W."""
+    W = words.shape[-1]
+    U = (W + 7) // 8
+    pad = np.zeros(words.shape[:-1] + (8 * U,), dtype=np.uint64)
+    pad[..., :W] = words
+    a = pad.reshape(words.shape[:-1] + (U, 8))
+    a = np.ascontiguousarray(np.swapaxes(a, -3, -2))  # [..., U, E, 8]
+    return torch.from_numpy(a.view(np.int64)).cuda()
 
 
 def D_np(D: torch.Tensor) -> np.ndarray:

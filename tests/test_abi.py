@@ -189,26 +189,27 @@ def host_binding(dl, monkeypatch):
 def test_binding_rejects_bad_tensors_before_any_call(host_binding):
     dl, torch = host_binding
     x = torch.zeros(100, 16)
-    bits = torch.zeros(1, 16, 2, dtype=torch.int64)
+    bits = torch.zeros(1, 1, 16, 8, dtype=torch.int64)  # N = 100: one 512-token unit of 16 experts
     D = torch.zeros(1, 16, 16, dtype=torch.int32)
     out = torch.zeros(1, 40, dtype=torch.uint8)
     bad = [
         lambda: dl.do_topk_signature(torch.zeros(100, 16, dtype=torch.float64), 2),     # score dtype
         lambda: dl.do_topk_signature(torch.zeros(4, 100, 16).transpose(1, 2), 2),      # not contiguous
         lambda: dl.do_topk_signature(torch.zeros(100), 2),                             # 1-D scores
-        lambda: dl.do_topk_signature(x, 2, bits=torch.zeros(1, 16, 1, dtype=torch.int64)),  # short bits
+        lambda: dl.do_topk_signature(x, 2, bits=torch.zeros(1, 1, 16, 7, dtype=torch.int64)),  # short bits
         lambda: dl.do_topk_signature(x, 2, bits=bits.int()),                           # bits dtype
         lambda: dl.do_fused(x, 2, bits=bits, D=torch.zeros(1, 16, 15, dtype=torch.int32), out=out),  # short D
         lambda: dl.do_fused(x, 2, D=D, out=torch.zeros(1, 39, dtype=torch.uint8)),     # short out
         lambda: dl.do_fused(x, 2, D=D.float(), out=out),                               # D dtype
-        lambda: dl.do_pairwise_hamming(bits, 200),                                     # N does not match W
+        lambda: dl.do_pairwise_hamming(bits, 600),                                     # N needs 2 units
+        lambda: dl.do_pairwise_hamming(torch.zeros(1, 1, 16, 4, dtype=torch.int64), 100),  # not 8 words per unit
         lambda: dl.do_pairwise_hamming(bits, 100, D=torch.zeros(1, 16, 8, dtype=torch.int32)),  # short D
         lambda: dl.do_loss(torch.zeros(16, 15, dtype=torch.int32)),                    # not square
         lambda: dl.do_loss(D, out=torch.zeros(1, 8, dtype=torch.uint8)),               # short out
-        lambda: dl.do_surrogate(x, 2, torch.zeros(1, 16, 1, dtype=torch.int64), D),    # short bits
+        lambda: dl.do_surrogate(x, 2, torch.zeros(1, 1, 16, 4, dtype=torch.int64), D),  # short bits
         lambda: dl.do_surrogate(x, 2, bits, torch.zeros(1, 8, 8, dtype=torch.int32)),  # short D
         lambda: dl.do_surrogate(x, 2, bits, D, grad=torch.zeros(100, 15)),             # short grad
-        lambda: dl.do_load_stats(bits, 200, 2),                                        # too few words for N
+        lambda: dl.do_load_stats(bits, 600, 2),                                        # too few units for N
         lambda: dl.do_load_stats(bits, 100, 2, p=torch.zeros(100, 15)),                # p of another E
         lambda: dl.do_load_stats(bits, 100, 2, expert_rank=[0] * 15, R=1),             # rank map length
         lambda: dl.do_load_stats(bits, 100, 2, loads=torch.zeros(1, 15, dtype=torch.int32)),  # short loads

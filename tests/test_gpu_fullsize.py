@@ -72,7 +72,7 @@ def test_workload2_full(dl, orc, syn):
     scores, _ = upload_workload(syn, 2, L)
     bits, D, out = dl.do_fused(scores, k, want_bits=True)
     torch.cuda.synchronize()
-    got_bits, got_D, recs = bits_np(bits), D_np(D), dl.loss_records(out)
+    got_bits, got_D, recs = bits_np(bits, N), D_np(D), dl.loss_records(out)
     for l in range(L):
         x = syn.workload_fill(2, l)
         F, ref_bits, ref_D, ref_L = orc.run(x, k)
@@ -104,7 +104,7 @@ def test_workload3_stream_full(dl, orc, syn):
             D, out = s.finalize()
             torch.cuda.synchronize()
             assert s.tokens == nmb * N
-            assert np.array_equal(bits_np(s.history()), ref_bits), f"rep {rep}: history differs"
+            assert np.array_equal(bits_np(s.history(), nmb * N), ref_bits), f"rep {rep}: history differs"
             np.testing.assert_array_equal(D_np(D), ref_D)
             loss_close(dl.loss_records(out)[0], ref_L)
     finally:
@@ -132,7 +132,7 @@ def test_workload4_full(dl, orc, syn):
     rng = np.random.default_rng(44)
     for l in range(L):
         print(f"[case] {w['name']} layer {l}: full oracle", flush=True)
-        words = bits_np(bits[l])
+        words = bits_np(bits[l], N)
         x = syn.workload_fill(4, l)
         F, ref_bits, ref_D, ref_L = orc.run(x, k)
         assert np.array_equal(words, ref_bits), f"layer {l}: signatures differ"
@@ -166,7 +166,7 @@ def test_more_than_2_31_tokens(dl, orc):
     bits, D, out = dl.do_fused(x, k, want_bits=True)
     torch.cuda.synchronize()
     W = (N + 63) // 64
-    b = bits.view(E, W)
+    b = bits[0].permute(1, 0, 2).reshape(E, -1)[:, :W]  # expert-major rows (a device copy of the unit-major layout)
     full = W - 1
     assert bool(torch.all((b[0, :full] ^ b[1, :full]) == -1)), "rows are not complements"
     assert bool(torch.all((b[0] & b[1]) == 0)), "a token selected both experts"
@@ -205,7 +205,8 @@ def test_maximum_layer_count(dl):
     x[100, 0, :] = -1.25  # a tie
     bits, D, out = dl.do_fused(x, k, want_bits=True)
     torch.cuda.synchronize()
-    b = bits.view(L, E).cpu().numpy()
+    b = bits[:, 0, :, 0].cpu().numpy()  # word 0 of each expert: [layer][unit 0][expert][word 0]
+    assert not bool(bits[:, 0, :, 1:].any()), "padding words of the last unit are not zero"
     want0 = (x[:, 0, 0] >= x[:, 0, 1]).cpu().numpy()
     assert np.array_equal(b[:, 0], want0.astype(np.int64)), "expert 0 bits"
     assert np.array_equal(b[:, 1], (~want0).astype(np.int64)), "expert 1 bits"

@@ -9,7 +9,7 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_util import to_dev
+from gpu_util import to_dev, units_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -51,7 +51,7 @@ CASES = [(1, 1, 1, 1), (100, 8, 2, 2), (4097, 64, 6, 1), (1000, 37, 5, 3), (777,
 def test_load_stats_match_oracle(dl, orc, syn, N, E, k, L, with_p, dtype):
     xs = [syn.normal(900 + 13 * E + l, N, E, 0) for l in range(L)]
     Fs = [orc.topk_signature(x, k) for x in xs]
-    bits = torch.from_numpy(np.stack([orc.pack(F) for F in Fs]).view(np.int64)).cuda()
+    bits = units_dev(np.stack([orc.pack(F) for F in Fs]))
     ps = [_probs(x, dtype) for x in xs] if with_p else None
     rng = np.random.default_rng(E + N)
     R = max(1, E // 4)
@@ -84,7 +84,7 @@ def test_load_stats_of_fused_signatures_and_empty_ranks(dl, orc, syn):
 
 
 def test_load_stats_of_a_stream_history(dl, orc, syn):
-    # the history rows are longer than ceil(N/64) words: ld = words per expert
+    # the history holds more units than ceil(N/512): ld = its padded words per expert
     E, k = 64, 6
     s = dl.DoStream(E, k, 50_000)
     mbs = [syn.normal(70 + b, n, E, 1) for b, n in enumerate([1000, 777, 4096])]

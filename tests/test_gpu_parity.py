@@ -7,7 +7,7 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_util import D_np, bits_np, loss_close, to_dev
+from gpu_util import D_np, bits_np, loss_close, to_dev, units_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -28,7 +28,7 @@ def _check_layer(dl, orc, scores_np, k, bits, D, rec, label=""):
     ref_D = orc.hamming(F)
     ref_L = orc.loss(ref_D)
     if bits is not None:
-        got = bits_np(bits)
+        got = bits_np(bits, scores_np.shape[0])
         if not np.array_equal(got, ref_bits):
             bad = np.argwhere(got != ref_bits)
             raise AssertionError(f"{label}: {len(bad)} signature words differ, first {bad[:4].tolist()}")
@@ -244,7 +244,7 @@ def test_multi_layer_batching_beyond_one_launch(dl, orc, syn):
     recs = dl.loss_records(fout)
     for l in (0, 1, 63, 64, 69):
         _check_layer(dl, orc, x[l], k, fb[l], fD[l], recs[l], f"layer {l}")
-    np.testing.assert_array_equal(bits_np(bits), bits_np(fb))
+    np.testing.assert_array_equal(bits_np(bits, N), bits_np(fb, N))
 
 
 def test_loss_of_arbitrary_matrices(dl):
@@ -305,7 +305,7 @@ def test_hamming_of_oracle_signatures(dl, orc, syn):
     x = syn.normal(12, 5000, 96, 1)
     F = orc.topk_signature(x, 7)
     words = orc.pack(F)
-    D = dl.do_pairwise_hamming(torch.from_numpy(words.view(np.int64)).cuda(), 5000)
+    D = dl.do_pairwise_hamming(units_dev(words), 5000)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(D_np(D)[0], orc.hamming(F))
 
@@ -457,7 +457,7 @@ def test_pairwise_hamming_of_stored_layers(dl, orc, syn, E, k, L, N, offset):
     words = np.stack([orc.pack(F) for F in Fs])
     big = torch.empty(L * E * E + offset, dtype=torch.int32, device="cuda")
     D = big[offset:].view(L, E, E)
-    dl.do_pairwise_hamming(torch.from_numpy(words.view(np.int64)).cuda(), N, D=D)
+    dl.do_pairwise_hamming(units_dev(words), N, D=D)
     torch.cuda.synchronize()
     got = D_np(D)
     for l in range(L):

@@ -46,7 +46,7 @@ def test_timed_fused_call_matches_untimed(dl, dtype):
     torch.cuda.synchronize()
     assert a.query() and b.query()
     assert 0.0 < a.elapsed_time(b) < 1000.0
-    np.testing.assert_array_equal(bits_np(b1), bits_np(b0))
+    np.testing.assert_array_equal(bits_np(b1, 7000), bits_np(b0, 7000))
     np.testing.assert_array_equal(D_np(D1), D_np(D0))
     assert dl.loss_records(o1) == dl.loss_records(o0)
 

@@ -10,7 +10,7 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_util import to_dev
+from gpu_util import to_dev, units_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -52,7 +52,7 @@ def _case(dl, orc, syn, seed, L, N, E, k, dtype, scale=1.0):
     bits = np.stack([orc.pack(F) for F in Fs])
     Ds = np.stack([orc.hamming(F) for F in Fs])
     p_dev = to_dev(np.concatenate(ps).reshape(L * N, E)).view(L, N, E)
-    b_dev = torch.from_numpy(bits.view(np.int64)).cuda()
+    b_dev = units_dev(bits)
     D_dev = torch.from_numpy(Ds.view(np.int32)).cuda()
     print(f"[case] surrogate L={L} N={N} E={E} k={k} dtype={dtype} scale={scale}", flush=True)
     loss, grad = dl.do_surrogate(p_dev, k, b_dev, D_dev, scale=scale)
@@ -83,7 +83,7 @@ def test_surrogate_without_gradient_output(dl, orc, syn):
     p = _probs(x, 0)
     F = orc.topk_signature(x, k)
     D = orc.hamming(F)
-    b = torch.from_numpy(orc.pack(F)[None].view(np.int64)).cuda()
+    b = units_dev(orc.pack(F)[None])
     Dd = torch.from_numpy(D[None].view(np.int32)).cuda()
     loss, grad = dl.do_surrogate(to_dev(p)[None], k, b, Dd, want_grad=False)
     torch.cuda.synchronize()
@@ -98,7 +98,7 @@ def test_surrogate_idle_expert_gradient_not_positive(dl, orc, syn):
     F = orc.topk_signature(x, k)
     D = orc.hamming(F)
     p = _probs(x, 0)
-    b = torch.from_numpy(orc.pack(F)[None].view(np.int64)).cuda()
+    b = units_dev(orc.pack(F)[None])
     Dd = torch.from_numpy(D[None].view(np.int32)).cuda()
     _, grad = dl.do_surrogate(to_dev(p)[None], k, b, Dd)
     g = grad[0].cpu().numpy()
@@ -120,7 +120,7 @@ def test_surrogate_general_signatures(dl, orc, syn, N, E):
     x = syn.normal(97, N, E, 0)
     p = _probs(x, 0)
     D = orc.hamming(F)
-    b = torch.from_numpy(orc.pack(F)[None].view(np.int64)).cuda()
+    b = units_dev(orc.pack(F)[None])
     Dd = torch.from_numpy(D[None].view(np.int32)).cuda()
     print(f"[case] surrogate general signatures N={N} E={E}", flush=True)
     loss, grad = dl.do_surrogate(to_dev(p)[None], k, b, Dd)

@@ -39,8 +39,8 @@ def _via_handle(dl, mbs, E, k):
 def _via_c_abi(dl, mbs, E, k):
     """The new entry point called through the C ABI directly (ctypes)."""
     n = mbs[0].shape[0]
-    W = (len(mbs) * n + 63) // 64
-    hist = torch.full((E, W), -1, dtype=torch.int64, device="cuda")  # garbage: the call must overwrite it
+    U = (len(mbs) * n + 511) // 512  # 512-token units of the signature layout
+    hist = torch.full((U, E, 8), -1, dtype=torch.int64, device="cuda")  # garbage: the call must overwrite it
     D = torch.full((E, E), -1, dtype=torch.int32, device="cuda")
     out = torch.zeros((1, 40), dtype=torch.uint8, device="cuda")
     ptrs = (ctypes.c_void_p * len(mbs))(*[t.data_ptr() for t in mbs])
