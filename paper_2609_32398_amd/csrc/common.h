@@ -10,6 +10,7 @@
 namespace dol {
 
 using u64 = unsigned long long;
+typedef unsigned long long v2u64 __attribute__((ext_vector_type(2)));  // 16-byte vector of two words
 
 constexpr int kWave = 64;
 constexpr int kFusedWaves = 8;                       // waves per block of the Top-K (+Gram) kernel

@@ -38,36 +38,55 @@ __device__ __forceinline__ V block_sum(V v, V* red) {
 // grid = (blocks per layer, layers).  Block b takes a contiguous range of the
 // layer's units (signature layout: a unit is the 8 words of every expert,
 // E * 8 contiguous words; words at or past W are not counted).  Thread t
-// reads words f = t + 256 i of every unit, expert f / 8, so its experts are
-// fixed: t / 8 + 32 i, i < NE.  The eight lanes of an expert then sum their
-// counts, and one of them adds the sum into loads (zeroed by the caller).
+// reads the word pairs f = t + 256 i of every unit with 16-byte loads (words
+// 2f, 2f + 1 of expert f / 4), so its experts are fixed: t / 4 + 64 i, i < NE;
+// two units are loaded before they are counted.  The four lanes of an expert
+// then sum their counts, and one of them adds the sum into loads (zeroed by
+// the caller).
 template <int NE>
 __global__ __launch_bounds__(kLsThreads) void k_unit_loads(const u64* bits, int64_t W, int64_t ld, int32_t E,
                                                            uint32_t* loads) {
-  static_assert(kLsThreads == 256, "experts t / 8 + 32 i");
-  const int l = blockIdx.y, t = threadIdx.x, s = t & 7;
+  static_assert(kLsThreads == 256, "experts t / 4 + 64 i");
+  const int l = blockIdx.y, t = threadIdx.x, s2 = 2 * (t & 3);  // the pair's first word in the unit
   const int64_t U = (W + 7) >> 3;
   const int64_t u0 = (int64_t)blockIdx.x * U / gridDim.x, u1 = (int64_t)(blockIdx.x + 1) * U / gridDim.x;
   const u64* lb = bits + (int64_t)l * E * ld;
   uint32_t c[NE];
 #pragma unroll
   for (int i = 0; i < NE; ++i) c[i] = 0u;
-  for (int64_t u = u0; u < u1; ++u) {
-    const u64* ub = lb + u * E * 8;
-    const bool wv = 8 * u + s < W;
+  auto count = [&](const v2u64& v, int64_t u, int i) {
+    const int64_t w = 8 * u + s2;
+    c[i] += (w < W ? (uint32_t)__popcll(v[0]) : 0u) + (w + 1 < W ? (uint32_t)__popcll(v[1]) : 0u);
+  };
+  int64_t u = u0;
+  for (; u + 1 < u1; u += 2) {
+    v2u64 va[NE], vb[NE];
 #pragma unroll
     for (int i = 0; i < NE; ++i) {
       const int f = t + kLsThreads * i;
-      if (wv && f < 8 * E) c[i] += (uint32_t)__popcll(__builtin_nontemporal_load(ub + f));
+      const bool in = f < 4 * E;
+      va[i] = in ? __builtin_nontemporal_load(reinterpret_cast<const v2u64*>(lb + u * E * 8) + f) : v2u64{0, 0};
+      vb[i] = in ? __builtin_nontemporal_load(reinterpret_cast<const v2u64*>(lb + (u + 1) * E * 8) + f) : v2u64{0, 0};
+    }
+#pragma unroll
+    for (int i = 0; i < NE; ++i) {
+      count(va[i], u, i);
+      count(vb[i], u + 1, i);
+    }
+  }
+  if (u < u1) {
+#pragma unroll
+    for (int i = 0; i < NE; ++i) {
+      const int f = t + kLsThreads * i;
+      if (f < 4 * E) count(__builtin_nontemporal_load(reinterpret_cast<const v2u64*>(lb + u * E * 8) + f), u, i);
     }
   }
 #pragma unroll
   for (int i = 0; i < NE; ++i) {
     c[i] += (uint32_t)__shfl_xor((int)c[i], 1);
     c[i] += (uint32_t)__shfl_xor((int)c[i], 2);
-    c[i] += (uint32_t)__shfl_xor((int)c[i], 4);
-    const int e = (t >> 3) + 32 * i;
-    if (s == 0 && e < E && c[i] != 0u) atomicAdd(&loads[(int64_t)l * E + e], c[i]);
+    const int e = (t >> 2) + 64 * i;
+    if ((t & 3) == 0 && e < E && c[i] != 0u) atomicAdd(&loads[(int64_t)l * E + e], c[i]);
   }
 }
 
@@ -209,7 +228,7 @@ hipError_t launch_load_stats(const u64* bits, int64_t N, int64_t ld, int32_t E, 
     const int64_t U = (W + 7) / 8;
     const int64_t per_layer = std::max<int64_t>(1, std::min<int64_t>(U, ((int64_t)di.cu_count * 4 + L - 1) / L));
     const dim3 grid((unsigned)per_layer, (unsigned)L);
-    const int ne = (E + 31) / 32;  // counters per thread
+    const int ne = (E + 63) / 64;  // counters per thread
     if (ne <= 1)
       hipLaunchKernelGGL(k_unit_loads<1>, grid, dim3(kLsThreads), 0, s, bits, W, ld, E, loads);
     else if (ne <= 2)
@@ -218,10 +237,8 @@ hipError_t launch_load_stats(const u64* bits, int64_t N, int64_t ld, int32_t E, 
       hipLaunchKernelGGL(k_unit_loads<4>, grid, dim3(kLsThreads), 0, s, bits, W, ld, E, loads);
     else if (ne <= 8)
       hipLaunchKernelGGL(k_unit_loads<8>, grid, dim3(kLsThreads), 0, s, bits, W, ld, E, loads);
-    else if (ne <= 16)
-      hipLaunchKernelGGL(k_unit_loads<16>, grid, dim3(kLsThreads), 0, s, bits, W, ld, E, loads);
     else
-      hipLaunchKernelGGL(k_unit_loads<32>, grid, dim3(kLsThreads), 0, s, bits, W, ld, E, loads);
+      hipLaunchKernelGGL(k_unit_loads<16>, grid, dim3(kLsThreads), 0, s, bits, W, ld, E, loads);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   if (p != nullptr) {

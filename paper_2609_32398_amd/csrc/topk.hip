@@ -702,8 +702,6 @@ __device__ __forceinline__ const unsigned char* word_rows(const Seg& sg, uint32_
   return sg.base + (uint64_t)(wl << 6) * (uint64_t)rowB;
 }
 
-typedef unsigned long long v2u64 __attribute__((ext_vector_type(2)));
-
 // ---------------------------------------------------------------------------
 // Top-K (+ Gram) kernel.  Work unit: 8 consecutive signature words (512
 // output positions) of one segment, starting 8-aligned within it; one unit
