@@ -416,6 +416,29 @@ def test_stream_finalize_between_appends_and_resets(dl, orc, syn, E, k, dtype):
         s.close()
 
 
+@pytest.mark.parametrize("E,k,sizes", [(128, 8, [1000, 4096, 333]), (40, 5, [64, 700]), (300, 8, [513, 1024])])
+def test_stream_history_prefix_is_a_signature_array(dl, orc, syn, E, k, sizes):
+    # the history's first ceil(tokens/512) units are the signature array of the
+    # appended tokens: do_pairwise_hamming over them gives the finalize's D
+    print(f"[case] history prefix E={E} k={k} sizes={sizes}", flush=True)
+    parts = [syn.normal(1500 + 11 * i + E, n, E, 1) for i, n in enumerate(sizes)]
+    s = dl.DoStream(E, k, 4 * sum(sizes))
+    try:
+        for p in parts:
+            s.append(to_dev(p))
+        N = s.tokens
+        D, _ = s.finalize()
+        hist = s.history()[: (N + 511) // 512].contiguous()
+        D2 = dl.do_pairwise_hamming(hist, N)
+        torch.cuda.synchronize()
+        _, words, ref_D, _ = orc.run_stream(parts, k)
+        np.testing.assert_array_equal(D_np(D2)[0], ref_D)
+        assert torch.equal(D2[0], D)
+        np.testing.assert_array_equal(bits_np(hist, N), words)
+    finally:
+        s.close()
+
+
 def test_stream_append_many_and_capacity(dl, orc, syn):
     E, k, nmb = 128, 8, 5
     parts = [syn.normal(900 + i, 777, E, 1) for i in range(nmb)]
