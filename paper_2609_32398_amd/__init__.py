@@ -290,6 +290,8 @@ def do_load_stats(bits: torch.Tensor, N: int, k: int, p: torch.Tensor | None = N
             raise ValueError(f"bits has {bits.shape[1]} units, fewer than ceil(N/512) = {_units(N)}")
         if ld == 0:
             ld = 8 * bits.shape[1]  # the tensor's layer stride
+        elif ld != 8 * bits.shape[1]:
+            raise ValueError(f"ld = {ld} differs from the tensor's {8 * bits.shape[1]} words per expert (0 takes it)")
         _want(bits, "bits", dtypes=_I64)
         ptr = bits.data_ptr()
         dev = bits.device

@@ -210,6 +210,7 @@ def test_binding_rejects_bad_tensors_before_any_call(host_binding):
         lambda: dl.do_surrogate(x, 2, bits, torch.zeros(1, 8, 8, dtype=torch.int32)),  # short D
         lambda: dl.do_surrogate(x, 2, bits, D, grad=torch.zeros(100, 15)),             # short grad
         lambda: dl.do_load_stats(bits, 600, 2),                                        # too few units for N
+        lambda: dl.do_load_stats(bits, 100, 2, ld=16),                                 # ld beyond the tensor
         lambda: dl.do_load_stats(bits, 100, 2, p=torch.zeros(100, 15)),                # p of another E
         lambda: dl.do_load_stats(bits, 100, 2, expert_rank=[0] * 15, R=1),             # rank map length
         lambda: dl.do_load_stats(bits, 100, 2, loads=torch.zeros(1, 15, dtype=torch.int32)),  # short loads
