@@ -19,6 +19,7 @@ import glob
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -94,11 +95,23 @@ def upload_workload(cfg: int, layers: int):
     return dev
 
 
+def _code_only(text: str, py: bool) -> str:
+    """The source without comments and blank lines (comments do not change the kernel)."""
+    if py:
+        text = re.sub(r'"""(?:.|\n)*?"""', "", text)
+        text = re.sub(r"(?m)#.*$", "", text)
+    else:
+        text = re.sub(r"/\*(?:.|\n)*?\*/", "", text)
+        text = re.sub(r"(?m)//.*$", "", text)
+    return "\n".join(l.rstrip() for l in text.splitlines() if l.strip())
+
+
 def kernel_source_digest() -> str:
+    """sha256 over the code of KERNEL_SOURCES (comments and blank lines removed)."""
     h = hashlib.sha256()
     for p in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, p), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, p), encoding="utf-8") as f:
+            h.update(_code_only(f.read(), p.endswith(".py")).encode())
     return h.hexdigest()
 
 

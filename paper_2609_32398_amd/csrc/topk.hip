@@ -13,7 +13,8 @@
 // issued before the current chunk is ranked, so each wave keeps one chunk in
 // flight at all times.  The 8 signature words of a step land in an LDS tile
 // (double-buffered) from which, during the next step, the block writes them
-// out as 64-byte runs per expert and feeds the Gram.
+// out and feeds the Gram.  Signatures are stored unit-major (sig_off): a
+// step's 8 words of every expert are one contiguous block of E * 64 bytes.
 //
 // Exact Top-K with composite 32-bit keys.  Each element becomes one signed
 // integer whose high bits order the score and whose low byte is (255 - expert
