@@ -133,14 +133,21 @@ def recorded_traffic(workload: str):
 def host_cpu():
     """CPU model and the CPUs this process may run on (the host of the GPU)."""
     model = "unknown"
+    ids = {}
     try:
         with open("/proc/cpuinfo") as f:
             for line in f:
-                if line.startswith("model name"):
+                key = line.split(":", 1)[0].strip()
+                if key == "model name" and model == "unknown":
                     model = line.split(":", 1)[1].strip()
+                elif key in ("cpu family", "model") and key not in ids:
+                    ids[key] = line.split(":", 1)[1].strip()
+                if model != "unknown" and len(ids) == 2:
                     break
     except OSError:
         pass
+    if ids:  # a virtualised host may name only the brand: add the family / model numbers
+        model = f"{model} (family {ids.get('cpu family', '?')}, model {ids.get('model', '?')})"
     try:
         avail = len(os.sched_getaffinity(0))
     except AttributeError:  # pragma: no cover
