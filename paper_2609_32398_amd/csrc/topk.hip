@@ -1237,9 +1237,10 @@ bool aligned_segments(const SegTable& tab, int rowB) {
 
 template <typename T, int EP>
 hipError_t launch_gm(const SegTable& tab, const PathArgs& a, bool fast, Sched sc, hipStream_t s, const ProfEv& pe) {
-  // the aligned specialization pays off up to 128 experts (bf16 workloads:
-  // -11 %); at 256 fp32 experts it measured 1 % slower, so it is not built there
-  if constexpr (EP <= 128) {
+  // the aligned specialization: bf16 at 128 experts -11 %; fp32 at 256 experts
+  // -8.5 % without signature output and -5 % with it where the stores are cheap
+  // (halved SGPR spills)
+  if constexpr (EP <= 256) {
     if (fast && aligned_segments(tab, a.E * (int)sizeof(T))) {
       if (a.cacc == nullptr) return launch_one<T, EP, kGramNone, true>(tab, a, fast, sc, s, pe);
       if (gram_mode() == kGramPopc) return launch_one<T, EP, kGramPopc, true>(tab, a, fast, sc, s, pe);

@@ -89,7 +89,9 @@ def test_random_shapes_normal(dl, orc, syn, E, k, N, dtype):
 # experts: fp32 rows of 32, 64, 96, 128 experts, bf16 rows of 64 and 128;
 # several layers, every entry point, normal and tie-heavy scores.
 @pytest.mark.parametrize("E,k,N,dtype", [(32, 1, 512, 0), (64, 8, 1536, 0), (96, 5, 2048, 0), (128, 8, 4608, 0),
-                                         (64, 6, 512, 1), (128, 8, 3584, 1), (128, 1, 1024, 1)])
+                                         (64, 6, 512, 1), (128, 8, 3584, 1), (128, 1, 1024, 1),
+                                         (160, 8, 1536, 0), (256, 8, 2048, 0), (256, 3, 512, 0),
+                                         (192, 5, 1024, 1), (256, 8, 2560, 1)])
 def test_unit_aligned_layers(dl, orc, syn, E, k, N, dtype):
     x = syn.normal(4000 + E + N, N, E, dtype)
     _run_all_entry_points(dl, orc, x, k, f"aligned normal E={E} k={k} N={N}")
