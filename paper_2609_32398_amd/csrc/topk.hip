@@ -1008,7 +1008,8 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
   // instructions per score) and switch for the rest of the kernel after
   // meeting a non-positive threshold; bf16 general keys cost ~1 more per
   // score, less than the exact re-rank a first non-positive threshold costs
-  // in a short launch, so bf16 starts with them.
+  // in a short launch, so bf16 rows start with them and move to positive
+  // keys within the row (below).
   bool gen = Traits<T>::kExact;
   int cb = 0;  // stage buffer holding the current chunk
   // key byte selectors, opaque to the compiler so that they stay in VGPRs
@@ -1074,6 +1075,7 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
         int rej = INT_MIN;
 #pragma unroll
         for (int i = 0; i < 8; ++i) top[i] = INT_MIN;
+        bool gk = gen;  // key kind of the next chunk of this row
         for (int c = 0; c < nch; ++c) {
           unsigned char* cur = st + cb * kChunkBytes;
           if (AL || c * 8 + 8 <= rowv) {
@@ -1091,10 +1093,18 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
             store_share(pbt);
             stored = true;
           }
-          if (gen)
+          if (gk)
             rank_chunk<T, true>(cur, lane, c * 8, ks, top, rej);
           else
             rank_chunk<T, false>(cur, lane, c * 8, ks, top, rej);
+          // bf16: once the 8th key of every token of the wave is a positive
+          // number, the rest of the row takes positive keys.  A negative score
+          // then keys below zero instead of at its general key, below that 8th
+          // key either way, and positive scores key the same under both kinds,
+          // so the list ends exactly as with general keys throughout.
+          if (Traits<T>::kExact && gk && c + 1 < nch &&
+              __ballot(valid && top[7] < Traits<T>::kPosMin) == 0ull)
+            gk = false;
           if (gram_done < kFusedWaves) {
             const int s_end = (((c + 1) * kFusedWaves) / nch) & ~(kGramStep - 1);
             gram_slots(pbt, gram_done, s_end);
