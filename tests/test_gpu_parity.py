@@ -192,6 +192,49 @@ def test_negative_and_bucket_ties_fp32(dl, orc, syn, dtype):
         _run_all_entry_points(dl, orc, bits.view(np.float32), 5, "bucket ties")
 
 
+def _key_switch_rows(seed):
+    """bf16 rows of 128 experts around the in-row switch to positive keys.
+
+    Scores come from a small set (many equal values, both zeros) and words of
+    64 tokens take turns: (0) every token has 12 positive scores among experts
+    0-63, so the wave switches after its first chunk; (1) as (0), but one token
+    has 5 positives there and 1 after, so its top-8 holds tied negative scores
+    and the wave must keep general keys; (2) 7 positives and a +0 among
+    experts 0-63 (the 8th key is not positive: no switch)."""
+    rng = np.random.default_rng(seed)
+    N, E = 64 * 24 + 37, 128
+    pos = np.array([0.25, 0.5, 1.0, 2.0, 3.0], np.float32)
+    neg = np.array([-8.0, -3.0, -2.5, -1.0, -0.5, -0.0], np.float32)
+    both = np.concatenate([pos, neg, np.array([0.0], np.float32)])
+    x = np.empty((N, E), np.float32)
+    for t in range(N):
+        w, lane = divmod(t, 64)
+        kind = w % 3
+        row = np.empty(E, np.float32)
+        npos = 12 if kind < 2 else 7
+        if kind == 1 and lane == (w * 7) % 64:
+            npos = 5
+        first = rng.choice(neg, 64)
+        first[rng.choice(64, npos, replace=False)] = rng.choice(pos, npos)
+        if kind == 2:
+            first[rng.choice(np.flatnonzero(first < 0), 1)] = 0.0
+        row[:64] = first
+        if kind == 1 and lane == (w * 7) % 64:
+            second = rng.choice(neg, 64)
+            second[rng.integers(64)] = rng.choice(pos)
+        else:
+            second = rng.choice(both, 64)
+        row[64:] = second
+        x[t] = row
+    return (x.view(np.uint32) >> 16).astype(np.uint16)
+
+
+@pytest.mark.parametrize("k", [8, 3])
+def test_bf16_rows_switching_to_positive_keys(dl, orc, k):
+    x = _key_switch_rows(77 + k)
+    _run_all_entry_points(dl, orc, x, k, f"bf16 key switch k={k}")
+
+
 def _bucket_tie_rows(rng, N, E, k, sign):
     """fp32 rows whose k-th and (k+1)-th largest values share their top 24
     bits: a cluster of 2..k+3 values b with random low bytes (some exactly
