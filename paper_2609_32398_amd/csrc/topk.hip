@@ -559,11 +559,12 @@ __device__ __forceinline__ void mfma_slots(typename Mfma<TS>::Acc (&acc)[kGP], c
   for (int s = s0; s < s1; s += Mfma<TS>::kWords) {  // not unrolled: keeps the fragment registers to one step's worth
     const int ws = s + (q >> 1);                      // the word this lane reads
     const uint32_t* w32 = reinterpret_cast<const uint32_t*>(bt + ws * stride);
+    // a fragment no active pair slot reads is left unset (the MFMAs below
+    // run only for active slots, whose tiles are all in need)
     v8i f[4];
 #pragma unroll
     for (int l = 0; l < 4; ++l)
-      f[l] = need[l] ? expand32_fp4(w32[(Mfma<TS>::expert(wt.tile[l], lane) ^ bt_swz(ws)) * 2 + (q & 1)])
-                     : v8i{0, 0, 0, 0, 0, 0, 0, 0};
+      if (need[l]) f[l] = expand32_fp4(w32[(Mfma<TS>::expert(wt.tile[l], lane) ^ bt_swz(ws)) * 2 + (q & 1)]);
 #pragma unroll
     for (int p = 0; p < kGP; ++p)
       if (wt.act & (1 << p)) acc[p] = Mfma<TS>::mac(f[slot_a(p)], f[slot_b(p)], acc[p]);
