@@ -1079,6 +1079,18 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
         bool gk = gen;  // key kind of the next chunk of this row
         for (int c = 0; c < nch; ++c) {
           unsigned char* cur = st + cb * kChunkBytes;
+          // Two waves share each SIMD and its arbiter prefers the older one:
+          // left to it, waves 0-3 end every unit early and wait at the block
+          // barrier (29 % of their time) while waves 4-7 finish alone.
+          // Waves 4-7 therefore take the higher priority for even chunks (bf16:
+          // after their share of the signature stores), which evens out when
+          // the two waves of a SIMD reach the barrier.
+          if (wave >= 4) {
+            if (c & 1)
+              __builtin_amdgcn_s_setprio(0);
+            else if constexpr (!Traits<T>::kExact)
+              __builtin_amdgcn_s_setprio(1);
+          }
           if (AL || c * 8 + 8 <= rowv) {
             DOL_WAIT_VMEM();  // this chunk's direct-to-LDS loads (and earlier stores) have completed
           } else {
@@ -1094,6 +1106,8 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
             store_share(pbt);
             stored = true;
           }
+          if constexpr (Traits<T>::kExact)
+            if (wave >= 4 && !(c & 1)) __builtin_amdgcn_s_setprio(1);
           if (gk)
             rank_chunk<T, true>(cur, lane, c * 8, ks, top, rej);
           else
@@ -1114,6 +1128,7 @@ __global__ __launch_bounds__(kFusedThreads) void k_topk(const SegTable tab_arg, 
           DOL_WAVE_FENCE();
           cb ^= 1;
         }
+        if (wave >= 4) __builtin_amdgcn_s_setprio(0);
         // the k-th and (k+1)-th keys: a wave-uniform branch on k, so that no
         // per-position predicate on k stays live (in registers) across the loop
         int sk, sk1;
