@@ -67,7 +67,8 @@ typedef enum {
   DO_ERR_UNSUPPORTED_DTYPE = 2, /* dtype is not DO_F32 or DO_BF16 */
   DO_ERR_CAPACITY = 3,          /* a stream append would exceed the history capacity */
   DO_ERR_OVERFLOW = 4,          /* E*(E-1)*N^2 >= 2^64 or N >= 2^32 */
-  DO_ERR_HIP = 5                /* the HIP runtime reported an error */
+  DO_ERR_HIP = 5,               /* the HIP runtime reported an error */
+  DO_ERR_NONFINITE = 6          /* a score is NaN (only with DO_OPT_CHECK_FINITE on) */
 } do_status;
 
 typedef enum { DO_F32 = 0, DO_BF16 = 1 } do_dtype;
@@ -355,19 +356,33 @@ do_status do_rem_dispatch(const do_rem_move* replicas, const int32_t* n_replicas
                           hipStream_t stream);
 
 /*
- * Process-wide overrides of internal choices that never change any result,
- * for tests and benchmarks (they take effect at the next call; calls already
+ * Process-wide options (they take effect at the next call; calls already
  * enqueued are unaffected).  Returns DO_ERR_INVALID_ARG for an unknown option
- * or a value out of range.
- *   DO_OPT_SCHEDULE  unit schedule of the score pass: -1 (default) measures
- *                    both candidates on the first launches of every shape of
- *                    at least 4 Mi tokens and keeps the faster; 0 fixes the
- *                    XCD-partitioned schedule; 1 fixes one contiguous range
- *                    of work units per block.
- *   DO_OPT_GRAM      co-occurrence Gram for E <= 256: 0 (default) the fp4
- *                    MFMA Gram, 1 the VALU popcount Gram.
+ * or a value out of range.  The first two override internal choices that
+ * never change any result, for tests and benchmarks:
+ *   DO_OPT_SCHEDULE      unit schedule of the score pass: -1 (default)
+ *                        measures both candidates on the first launches of
+ *                        every shape of at least 512 Ki tokens (1,024 units)
+ *                        and keeps the faster; 0 fixes the XCD-partitioned
+ *                        schedule; 1 fixes one contiguous range of work units
+ *                        per block.
+ *   DO_OPT_GRAM          co-occurrence Gram for E <= 256: 0 (default) the fp4
+ *                        MFMA Gram, 1 the VALU popcount Gram.
+ * The third adds an input check.  NaN scores have a defined rank (below -inf,
+ * equal to each other), so results are defined without it:
+ *   DO_OPT_CHECK_FINITE  0 (default) off; 1: do_topk_signature, do_fused,
+ *                        do_stream_append and do_stream_append_many first scan
+ *                        their scores for NaN (+-inf are ordinary values), wait
+ *                        for the scan on the caller's stream, and return
+ *                        DO_ERR_NONFINITE without writing anything (the
+ *                        stream handle is unchanged) if one is found.  Such a
+ *                        call synchronises the stream, so under stream capture
+ *                        it returns DO_ERR_INVALID_ARG.  Check-mode calls of
+ *                        one process are serialised by a host lock.
+ *                        do_global_batch_noalloc, whose callers cannot wait,
+ *                        does not scan.
  */
-typedef enum { DO_OPT_SCHEDULE = 0, DO_OPT_GRAM = 1 } do_option;
+typedef enum { DO_OPT_SCHEDULE = 0, DO_OPT_GRAM = 1, DO_OPT_CHECK_FINITE = 2 } do_option;
 do_status do_set_option(do_option opt, int32_t value);
 
 /* Text of a status code, and the message of the calling thread's last error. */

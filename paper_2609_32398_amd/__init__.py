@@ -27,9 +27,9 @@ import torch
 
 from .hipbuild import LIB_PATH, build  # noqa: F401
 
-DO_OK, DO_ERR_INVALID_ARG, DO_ERR_UNSUPPORTED_DTYPE, DO_ERR_CAPACITY, DO_ERR_OVERFLOW, DO_ERR_HIP = range(6)
+DO_OK, DO_ERR_INVALID_ARG, DO_ERR_UNSUPPORTED_DTYPE, DO_ERR_CAPACITY, DO_ERR_OVERFLOW, DO_ERR_HIP, DO_ERR_NONFINITE = range(7)
 DO_F32, DO_BF16 = 0, 1
-DO_OPT_SCHEDULE, DO_OPT_GRAM = 0, 1
+DO_OPT_SCHEDULE, DO_OPT_GRAM, DO_OPT_CHECK_FINITE = 0, 1, 2
 
 LOSS_RESULT_BYTES = 40
 LOSS_FIELDS = ("sum", "sumsq", "loss", "mean", "var")
@@ -166,8 +166,9 @@ def _units(N: int) -> int:
 
 
 def set_option(option: int, value: int):
-    """do_set_option: process-wide override of a choice that never changes results
-    (DO_OPT_SCHEDULE: -1 tuned, 0 XCD-partitioned, 1 contiguous; DO_OPT_GRAM: 0 MFMA, 1 popcount)."""
+    """do_set_option: process-wide options (DO_OPT_SCHEDULE: -1 tuned, 0 XCD-partitioned,
+    1 contiguous; DO_OPT_GRAM: 0 MFMA, 1 popcount; DO_OPT_CHECK_FINITE: 1 makes the
+    score-ranking calls fail with DO_ERR_NONFINITE on a NaN score, 0 turns it off)."""
     _check(lib().do_set_option(int(option), int(value)), "do_set_option")
 
 

@@ -1,6 +1,7 @@
 // Host side of the C ABI declared in include/doloss.h: argument validation,
 // dispatch to the kernels, and the streaming-history handles.
 #include <algorithm>
+#include <atomic>
 #include <cstring>
 #include <mutex>
 #include <new>
@@ -128,6 +129,51 @@ do_status run_layers(const void* scores, do_dtype dt, int64_t N, int32_t E, int3
 
 }  // namespace
 
+// ---------------------------------------------------------------------------
+// Check-finite mode (do_set_option DO_OPT_CHECK_FINITE): the calls that rank
+// scores first scan them for NaN into a one-word flag, read it back and fail
+// before any other launch.  The flag is a file-scope device variable whose
+// address is looked up once per device; the scan, the copy and the wait run
+// under one host lock, so check-mode calls of a process never share the flag.
+// ---------------------------------------------------------------------------
+static __device__ uint32_t nan_flag;
+
+namespace {
+
+constexpr int kFlagDevices = 64;
+std::atomic<int> g_check_finite{0};
+std::mutex g_flag_mu;
+uint32_t* g_flag_ptr[kFlagDevices] = {};
+
+do_status check_finite(const void* const* xs, int32_t count, int64_t elems_each, do_dtype dt, hipStream_t s) {
+  if (g_check_finite.load(std::memory_order_relaxed) == 0) return DO_OK;
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  DO_TRY(hip_status(hipStreamIsCapturing(s, &cs), "hipStreamIsCapturing"));
+  if (cs != hipStreamCaptureStatusNone)
+    return fail(DO_ERR_INVALID_ARG, "the check-finite mode waits for its scan and cannot run under stream capture");
+  int dev = -1;
+  DO_TRY(hip_status(hipGetDevice(&dev), "hipGetDevice"));
+  if (dev < 0 || dev >= kFlagDevices) return fail(DO_ERR_INVALID_ARG, "device index beyond 63");
+  std::lock_guard<std::mutex> lock(g_flag_mu);
+  if (g_flag_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    DO_TRY(hip_status(hipGetSymbolAddress(&p, HIP_SYMBOL(nan_flag)), "hipGetSymbolAddress(nan_flag)"));
+    if (p == nullptr) return fail(DO_ERR_HIP, "hipGetSymbolAddress(nan_flag) returned NULL");
+    g_flag_ptr[dev] = static_cast<uint32_t*>(p);
+  }
+  uint32_t* flag = g_flag_ptr[dev];
+  DO_TRY(hip_status(dol::launch_fill_u32(flag, 1, 0u, s), "flag clear"));
+  for (int32_t i = 0; i < count; ++i)
+    DO_TRY(hip_status(dol::launch_nan_scan(xs[i], (int32_t)dtype_size(dt), elems_each, flag, s), "NaN scan"));
+  uint32_t seen = 0;
+  DO_TRY(hip_status(hipMemcpyAsync(&seen, flag, sizeof(seen), hipMemcpyDeviceToHost, s), "flag copy"));
+  DO_TRY(hip_status(hipStreamSynchronize(s), "hipStreamSynchronize"));
+  if (seen != 0u) return fail(DO_ERR_NONFINITE, "the scores hold a NaN (check-finite mode); nothing was written");
+  return DO_OK;
+}
+
+}  // namespace
+
 // Copies of a stream's co-occurrence counters (block b of an append adds its
 // counts into copy b % kStreamCopies).  Eight copies, one per XCD, were
 // measured: the append kernel took the same time at workload 3 and the
@@ -163,6 +209,7 @@ DOLOSS_API const char* do_status_string(do_status s) {
     case DO_ERR_CAPACITY: return "DO_ERR_CAPACITY";
     case DO_ERR_OVERFLOW: return "DO_ERR_OVERFLOW";
     case DO_ERR_HIP: return "DO_ERR_HIP";
+    case DO_ERR_NONFINITE: return "DO_ERR_NONFINITE";
   }
   return "DO_ERR_UNKNOWN";
 }
@@ -172,6 +219,11 @@ DOLOSS_API const char* do_last_error(void) { return g_last_error.c_str(); }
 DOLOSS_API int32_t do_version(void) { return 100; }
 
 DOLOSS_API do_status do_set_option(do_option opt, int32_t value) {
+  if (opt == DO_OPT_CHECK_FINITE) {
+    if (value != 0 && value != 1) return fail(DO_ERR_INVALID_ARG, "DO_OPT_CHECK_FINITE takes 0 or 1");
+    g_check_finite.store(value, std::memory_order_relaxed);
+    return DO_OK;
+  }
   if (!dol::set_option((int)opt, value)) return fail(DO_ERR_INVALID_ARG, "unknown option or value out of range");
   return DO_OK;
 }
@@ -189,6 +241,7 @@ DOLOSS_API do_status do_topk_signature(const void* scores, do_dtype dtype, int64
   DO_TRY(check_k(k, E));
   DO_TRY(check_scores(scores, dtype));
   if (bits == nullptr || !aligned(bits, 8)) return fail(DO_ERR_INVALID_ARG, "bits is NULL or not 8-byte aligned");
+  DO_TRY(check_finite(&scores, 1, N * E * L, dtype, stream));
   return run_layers(scores, dtype, N, E, k, L, reinterpret_cast<u64*>(bits), nullptr, stream);
 }
 
@@ -225,6 +278,7 @@ DOLOSS_API do_status do_fused(const void* scores, do_dtype dtype, int64_t N, int
   if (out == nullptr || !aligned(out, 8)) return fail(DO_ERR_INVALID_ARG, "out is NULL or not 8-byte aligned");
   if (E > dol::kFastMaxE && bits == nullptr)
     return fail(DO_ERR_INVALID_ARG, "do_fused needs a bits buffer when E > 256");
+  DO_TRY(check_finite(&scores, 1, N * E * L, dtype, stream));
   DO_TRY(hip_status(dol::launch_fill_u32(D, (int64_t)L * E * E, 0u, stream), "fill"));
   if (E <= dol::kFastMaxE) {
     DO_TRY(run_layers(scores, dtype, N, E, k, L, reinterpret_cast<u64*>(bits), D, stream));
@@ -434,6 +488,7 @@ do_status stream_append(do_stream* h, const void* const* scores, do_dtype dtype,
   }
   if ((h->capacity - h->tokens) / count < n)
     return fail(DO_ERR_CAPACITY, "append would exceed the history capacity");
+  DO_TRY(check_finite(scores, count, n * h->E, dtype, stream));
   // Words that this append writes.  When the micro-batches start and end on
   // word boundaries every word is written whole by exactly one of them, with
   // plain stores.  Otherwise words shared between micro-batches are OR-ed, so

@@ -86,6 +86,9 @@ DevInfo device_info();
 
 hipError_t launch_fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s);
 hipError_t launch_fill_u64(u64* p, int64_t n, hipStream_t s);
+// Sets *flag to 1 when any of the n elements at x (fp32 or bf16 bit patterns,
+// elem_bytes 4 or 2, x aligned to its element size) is a NaN; else leaves it.
+hipError_t launch_nan_scan(const void* x, int32_t elem_bytes, int64_t n, uint32_t* flag, hipStream_t s);
 // Zeroes signature words [w0, w0 + nw) of all E experts of one layer at p.
 hipError_t launch_fill_sig_words(u64* p, int32_t E, int64_t w0, int64_t nw, hipStream_t s);
 

@@ -24,6 +24,41 @@ __global__ void k_fill_u32(uint32_t* p, int64_t n, uint32_t v) {
     p[i] = v;
 }
 
+// NaN scan of the check-finite mode: *flag = 1 when any of the n elements
+// (fp32 or bf16 bit patterns of elem_bytes 4 or 2) is a NaN.  The magnitude
+// bits of a NaN exceed those of infinity, and one add per 32-bit word moves
+// that comparison into each element's sign position: (w & 0x7FFFFFFF) +
+// 0x007FFFFF carries into bit 31 exactly when w & 0x7FFFFFFF > 0x7F800000, and
+// two bf16 halves do the same with 0x7FFF7FFF and 0x007F007F (a half's sum
+// stays below 0x10000, so nothing carries into the other half).
+__global__ void k_nan_scan(const unsigned char* x, int eb, int64_t n, uint32_t* flag) {
+  typedef uint32_t v4w __attribute__((ext_vector_type(4)));
+  const uint32_t mag = eb == 4 ? 0x7FFFFFFFu : 0x7FFF7FFFu;
+  const uint32_t add = eb == 4 ? 0x007FFFFFu : 0x007F007Fu;
+  const uint32_t top = eb == 4 ? 0x80000000u : 0x80008000u;
+  auto nan_in = [&](uint32_t w) { return ((w & mag) + add) & top; };
+  auto elem = [&](int64_t e) {
+    return eb == 4 ? reinterpret_cast<const uint32_t*>(x)[e] : (uint32_t)reinterpret_cast<const uint16_t*>(x)[e];
+  };
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t bytes = n * eb;
+  // x is aligned to its element size, so the bytes before the first 16-byte
+  // boundary and after the last one are whole elements
+  int64_t head = (int64_t)((16 - (reinterpret_cast<uintptr_t>(x) & 15)) & 15);
+  if (head > bytes) head = bytes;
+  const int64_t nv = (bytes - head) / 16;
+  const v4w* v = reinterpret_cast<const v4w*>(x + head);
+  uint32_t any = 0;
+  for (int64_t i = i0; i < nv; i += stride) {
+    const v4w q = __builtin_nontemporal_load(v + i);
+    any |= nan_in(q.x) | nan_in(q.y) | nan_in(q.z) | nan_in(q.w);
+  }
+  for (int64_t e = i0; e < head / eb; e += stride) any |= nan_in(elem(e));
+  for (int64_t e = (head + nv * 16) / eb + i0; e < n; e += stride) any |= nan_in(elem(e));
+  if (any != 0u) *flag = 1u;
+}
+
 // Zeroes n words; 16-byte stores when p is 16-byte aligned.
 __global__ void k_fill_u64(u64* p, int64_t n) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
@@ -496,6 +531,15 @@ hipError_t launch_fill_u32(uint32_t* p, int64_t n, uint32_t v, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   const int64_t blocks = std::min<int64_t>((n + 255) / 256, 4096);
   hipLaunchKernelGGL(k_fill_u32, dim3((unsigned)blocks), dim3(256), 0, s, p, n, v);
+  return hipGetLastError();
+}
+
+hipError_t launch_nan_scan(const void* x, int32_t elem_bytes, int64_t n, uint32_t* flag, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const int64_t nv = n * elem_bytes / 16 + 1;
+  const int64_t blocks = std::min<int64_t>((nv + 255) / 256, 2048);
+  hipLaunchKernelGGL(k_nan_scan, dim3((unsigned)blocks), dim3(256), 0, s, static_cast<const unsigned char*>(x),
+                     (int)elem_bytes, n, flag);
   return hipGetLastError();
 }
 

@@ -49,6 +49,8 @@ def test_status_strings_and_version(dl):
     L = dl.lib()
     assert L.do_status_string(0) == b"DO_OK"
     assert L.do_status_string(3) == b"DO_ERR_CAPACITY"
+    assert L.do_status_string(6) == b"DO_ERR_NONFINITE"
+    assert dl.DO_ERR_NONFINITE == 6 and dl.DO_OPT_CHECK_FINITE == 2
     assert L.do_version() >= 100
 
 
@@ -246,8 +248,11 @@ def test_set_option_rejects_unknown_values(dl):
     assert L.do_set_option(0, 2) == 1     # schedule index out of range
     assert L.do_set_option(0, -2) == 1
     assert L.do_set_option(1, 2) == 1     # gram kind out of range
+    assert L.do_set_option(2, 2) == 1     # the check-finite mode is 0 or 1
+    assert L.do_set_option(2, -1) == 1
     assert L.do_set_option(0, -1) == 0    # the defaults are accepted (and leave the state as it was)
     assert L.do_set_option(1, 0) == 0
+    assert L.do_set_option(2, 0) == 0
 
 
 def test_fused_without_bits_needs_e_at_most_256(dl):
