@@ -349,7 +349,8 @@ def bench_layers(args, cfg):
                        bytes_per_token=s_bytes // tokens, achieved_gbs=s_bytes / (s_ms / 1e3) / 1e9,
                        frac=s_bytes / (s_ms / 1e3) / 1e9 / HBM_PEAK_GBS,
                        tokens_per_s=tokens / (s_ms / 1e3)),
-        load_stats=dict(kernels="k_unit_loads + k_lbl_sums + k_load_finalize (loads, Local-LBL, MaxVio)",
+        load_stats=dict(kernels="k_unit_loads + " + ("k_lbl_sums_vec" if w["dtype"] == 0 else "k_lbl_sums")
+                        + " + k_load_finalize (loads, Local-LBL, MaxVio)",
                         ms=ls_ms, algorithmic_bytes=ls_bytes, bytes_per_token=ls_bytes // tokens,
                         achieved_gbs=ls_bytes / (ls_ms / 1e3) / 1e9,
                         frac=ls_bytes / (ls_ms / 1e3) / 1e9 / HBM_PEAK_GBS,
